@@ -1,0 +1,114 @@
+/*
+ * libsteel -- sparsity-aware fused attention forward for AMD Instinct MI355X
+ * (gfx950).  C ABI: plain pointers and sizes, no C++ or framework types.
+ *
+ * What it computes (Section II-A, Eq. 1 of the STEEL paper, with the masking
+ * of Section IV-A):  for every batch b and query head h, with key/value head
+ * g = h / (Hq / Hkv),
+ *
+ *     O[b,h,i,:] = sum_j softmax_j( scale * Q[b,h,i,:] . K[b,g,j,:] + M[b,h,i,j] ) V[b,g,j,:]
+ *
+ * where M is 0 where element (i, j) is visible and -inf elsewhere.  (i, j) is
+ * visible iff its 64x64 block (i/64, j/64) is live in ``block_mask`` and, when
+ * ``causal`` is nonzero, j <= i + (S_k - S_q) (bottom-right aligned causal
+ * structure; plain lower-triangular when S_q == S_k).  A query row with no
+ * visible key has output 0.
+ *
+ * The pass is fused (Section II-A; Algorithm 1): scores, the running row
+ * maximum and row sum, and the rescaled accumulation of P.V stay on chip; only
+ * Q, K, V, the mask and O touch device memory.  Key blocks that are dead
+ * (mask byte 0, or entirely above the causal diagonal) are never loaded;
+ * partially masked blocks get the element mask from their coordinates;
+ * unmasked blocks run without it (the three tile cases of Section IV-A).
+ *
+ * All calls are asynchronous on the given HIP stream (a hipStream_t passed as
+ * ``void*``; NULL means the default stream) and return once the work is
+ * enqueued.  Argument checks run before any HIP call; on a non-OK status
+ * nothing has been enqueued and no output has been written.  Kernel faults
+ * surface at the caller's next synchronisation, as usual for HIP.
+ *
+ * Thread safety: calls may be made concurrently from several threads and on
+ * several streams; the only process-wide state is a per-device memory pool
+ * for internal workspace and the thread-local error text.
+ */
+#ifndef STEEL_H
+#define STEEL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum steel_status {
+  STEEL_OK = 0,
+  STEEL_ERR_INVALID_ARGUMENT = 1, /* bad pointer, shape, alignment or scale    */
+  STEEL_ERR_UNSUPPORTED = 2,      /* valid but not built: D not 64/128, blk != 64 */
+  STEEL_ERR_HIP = 3               /* HIP runtime error; see steel_last_error()  */
+} steel_status;
+
+/*
+ * Fused attention forward (Section II-A Eq. 1; Algorithm 1; Section IV-A).
+ *
+ *   q          bf16 [B][Hq][S_q][D], device memory, row-major, 16-byte aligned
+ *   k, v       bf16 [B][Hkv][S_k][D], device memory, row-major, 16-byte aligned
+ *   block_mask uint8 [B][Hq][ceil(S_q/blk)][ceil(S_k/blk)], device memory,
+ *              nonzero = live block; NULL = every block live
+ *   out        fp32 [B][Hq][S_q][D], device memory, 16-byte aligned; every
+ *              element is written
+ *   B, Hq, Hkv, S_q, S_k >= 1;  Hq % Hkv == 0
+ *   D          head dimension: 64 or 128 (others: STEEL_ERR_UNSUPPORTED)
+ *   blk        block edge of the mask: 64 (others: STEEL_ERR_UNSUPPORTED)
+ *   scale      multiplies Q.K^T; finite and > 0 (1/sqrt(D) in the paper)
+ *   causal     0 or 1
+ *   stream     hipStream_t as void*, or NULL
+ *
+ * Inputs and output are owned by the caller; the library keeps no pointer to
+ * them after it returns.  Internal workspace (the compressed live-block list
+ * and the work order) is taken stream-ordered from a per-device pool and
+ * released stream-ordered.  Results are bitwise reproducible run to run.
+ */
+int steel_attn_fwd(const void* q, const void* k, const void* v,
+                   const uint8_t* block_mask, void* out,
+                   int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                   float scale, int causal, void* stream);
+
+/*
+ * Live-block index (Section IV-A tile classes, as a compressed list; Section
+ * IV-C balance, as a work order).  Rows are r = (b*Hq + h)*nQB + qb with
+ * nQB = ceil(S_q/blk), nKB = ceil(S_k/blk).
+ *
+ *   A block (qb, kb) is dead if its mask byte is 0, or if causal and
+ *   kb*blk > min((qb+1)*blk, S_q) - 1 + (S_k - S_q).  A live block is partial
+ *   if causal and (kb+1)*blk - 1 > qb*blk + (S_k - S_q), or if
+ *   (kb+1)*blk > S_k.
+ *
+ *   row_ptr  int32 [R+1], device: exclusive prefix sum of the live counts
+ *   col      uint32 [capacity], device: for row r, entries
+ *            row_ptr[r] .. row_ptr[r+1]-1 hold the live kb in increasing
+ *            order, bit 31 set for a partial block.  Capacity must be at
+ *            least R*nKB (the live total is only known on the device).
+ *   order    int32 [R], device: the rows sorted by live count, heaviest
+ *            first, equal counts in increasing row order.  When nKB >= 4096
+ *            the count is first divided by the smallest power of two that
+ *            brings it below 4096.
+ *
+ * The arguments shared with steel_attn_fwd mean the same and are checked the
+ * same way; D and the tensors are not needed here.
+ */
+int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k,
+                      int blk, int causal, int32_t* row_ptr, uint32_t* col,
+                      int32_t* order, void* stream);
+
+/* Text of the last non-OK status returned on the calling thread ("" if none). */
+const char* steel_last_error(void);
+
+/* Library version string. */
+const char* steel_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STEEL_H */

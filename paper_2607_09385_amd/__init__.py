@@ -1,0 +1,113 @@
+"""libsteel: sparsity-aware fused attention forward on MI355X (gfx950).
+
+``attn_fwd`` computes softmax(Q K^T * scale + mask) V in one fused pass over
+64x64 tiles, visiting only the key blocks that the block mask and the causal
+structure leave live (the STEEL paper: Section II-A Eq. 1, Algorithm 1,
+Section IV-A).  ``block_index`` exposes the compressed live-block list and the
+heaviest-first work order the pass walks.
+
+PyTorch provides device memory and the current stream; all arithmetic runs in
+the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional
+
+from . import _lib
+from ._lib import SteelError, load, last_error, version  # noqa: F401
+
+BLK = 64
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _check_bf16(name, t, ndim=4):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a GPU device (got {t.device})")
+    if t.dtype != torch.bfloat16:
+        raise ValueError(f"{name} must be bfloat16 (got {t.dtype})")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims [B, H, S, D] (got {tuple(t.shape)})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal: bool = True,
+             blk: int = BLK, out=None, stream=None):
+    """Fused masked attention forward.
+
+    q: bf16 [B, Hq, S_q, D]; k, v: bf16 [B, Hkv, S_k, D]; block_mask: uint8
+    [B, Hq, ceil(S_q/blk), ceil(S_k/blk)] or None (all live).  Returns fp32
+    [B, Hq, S_q, D] (or fills ``out``).  Asynchronous on the current stream.
+    """
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_bf16(name, t)
+    B, Hq, S_q, D = q.shape
+    Bk, Hkv, S_k, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Bk != B or Dk != D:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    if q.device != k.device or q.device != v.device:
+        raise ValueError("q, k and v must be on the same device")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    mask_ptr = None
+    if block_mask is not None:
+        nQB, nKB = -(-S_q // blk), -(-S_k // blk)
+        if not isinstance(block_mask, torch.Tensor) or block_mask.dtype != torch.uint8:
+            raise ValueError("block_mask must be a uint8 torch.Tensor")
+        if tuple(block_mask.shape) != (B, Hq, nQB, nKB):
+            raise ValueError(f"block_mask must be [{B}, {Hq}, {nQB}, {nKB}] (got {tuple(block_mask.shape)})")
+        if block_mask.device != q.device or not block_mask.is_contiguous():
+            raise ValueError("block_mask must be contiguous and on q's device")
+        mask_ptr = block_mask.data_ptr()
+    if out is None:
+        out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+    else:
+        if out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
+            raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+    with torch.cuda.device(q.device):
+        st = _lib.load().steel_attn_fwd(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(),
+            B, Hq, Hkv, S_q, S_k, D, blk, float(scale), 1 if causal else 0, _stream_handle(stream))
+    _lib.check(st)
+    return out
+
+
+def block_index(block_mask, B: int, Hq: int, S_q: int, S_k: int, *, causal: bool = True,
+                blk: int = BLK, device=None, stream=None):
+    """Live-block list: returns (row_ptr int32 [R+1], col int32 [R*nKB]
+    (valid up to row_ptr[-1]; bit 31 = partial), order int32 [R])."""
+    torch = _torch()
+    nQB, nKB = -(-S_q // blk), -(-S_k // blk)
+    R = B * Hq * nQB
+    if block_mask is not None:
+        if block_mask.dtype != torch.uint8 or tuple(block_mask.shape) != (B, Hq, nQB, nKB):
+            raise ValueError("block_mask must be uint8 [B, Hq, nQB, nKB]")
+        if not block_mask.is_contiguous() or block_mask.device.type != "cuda":
+            raise ValueError("block_mask must be a contiguous GPU tensor")
+        device = block_mask.device
+    device = device or torch.device("cuda")
+    row_ptr = torch.empty(R + 1, dtype=torch.int32, device=device)
+    col = torch.empty(max(R * nKB, 1), dtype=torch.int32, device=device)
+    order = torch.empty(R, dtype=torch.int32, device=device)
+    with torch.cuda.device(device):
+        st = _lib.load().steel_block_index(
+            None if block_mask is None else block_mask.data_ptr(), B, Hq, S_q, S_k, blk,
+            1 if causal else 0, row_ptr.data_ptr(), col.data_ptr(), order.data_ptr(),
+            _stream_handle(stream))
+    _lib.check(st)
+    return row_ptr, col, order

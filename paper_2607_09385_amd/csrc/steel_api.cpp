@@ -1,0 +1,236 @@
+// C ABI of libsteel: argument checks, workspace, launches.
+//
+// Every check runs before the first HIP call, so an invalid call enqueues
+// nothing and writes no output.  Workspace for the live-block index comes
+// from a per-device stream-ordered memory pool (kept across calls, never
+// trimmed), so a call stays asynchronous and may overlap calls on other
+// streams.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <mutex>
+#include <string>
+
+#include "../../include/steel.h"
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(STEEL_ERR_HIP, "HIP error in %s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+constexpr int kMaxDevices = 64;
+std::mutex g_pool_mu;
+hipMemPool_t g_pools[kMaxDevices] = {};
+
+hipError_t device_pool(int dev, hipMemPool_t* out) {
+  std::lock_guard<std::mutex> lk(g_pool_mu);
+  if (!g_pools[dev]) {
+    hipMemPoolProps props = {};
+    props.allocType = hipMemAllocationTypePinned;
+    props.handleTypes = hipMemHandleTypeNone;
+    props.location.type = hipMemLocationTypeDevice;
+    props.location.id = dev;
+    hipMemPool_t pool = nullptr;
+    hipError_t e = hipMemPoolCreate(&pool, &props);
+    if (e != hipSuccess) return e;
+    uint64_t keep = UINT64_MAX;
+    e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+    if (e != hipSuccess) {
+      (void)hipMemPoolDestroy(pool);
+      return e;
+    }
+    g_pools[dev] = pool;
+  }
+  *out = g_pools[dev];
+  return hipSuccess;
+}
+
+// Shape checks shared by both entry points; fills the Problem on success.
+int check_shape(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
+                steel::Problem* p) {
+  if (B < 1 || Hq < 1 || Hkv < 1 || S_q < 1 || S_k < 1)
+    return fail(STEEL_ERR_INVALID_ARGUMENT,
+                "sizes must be >= 1 (B=%d Hq=%d Hkv=%d S_q=%d S_k=%d)", B, Hq, Hkv, S_q, S_k);
+  if (Hq % Hkv != 0)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (causal != 0 && causal != 1)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "causal must be 0 or 1 (got %d)", causal);
+  if (blk != steel::kBlk)
+    return fail(STEEL_ERR_UNSUPPORTED, "blk=%d not supported (only %d)", blk, steel::kBlk);
+  const long long nQB = (S_q + (long long)blk - 1) / blk;
+  const long long nKB = (S_k + (long long)blk - 1) / blk;
+  const long long R = (long long)B * Hq * nQB;
+  if (R > INT32_MAX / 2 || R * nKB >= (1ll << 31))
+    return fail(STEEL_ERR_UNSUPPORTED,
+                "block grid too large: %lld rows x %lld key blocks exceeds 2^31 list entries", R,
+                nKB);
+  p->B = B;
+  p->Hq = Hq;
+  p->Hkv = Hkv;
+  p->S_q = S_q;
+  p->S_k = S_k;
+  p->G = Hq / Hkv;
+  p->nQB = (int)nQB;
+  p->nKB = (int)nKB;
+  p->causal = causal;
+  p->delta = S_k - S_q;
+  p->R = (int)R;
+  int shift = 0;
+  while (((p->nKB >> shift) + 1) > steel::kMaxBins) ++shift;
+  p->bin_shift = shift;
+  p->nbins = (p->nKB >> shift) + 1;
+  p->pack = 1;
+  p->NP = 0;
+  return STEEL_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  size_t cnt, uni, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, total;
+};
+
+Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
+  Layout L{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  const size_t nch_s = steel::nchunks(p.R);
+  const size_t nch_p = p.pack > 1 ? steel::nchunks(p.NP) : 0;
+  L.cnt = take(sizeof(int32_t) * p.R);
+  L.uni = take(p.NP > 0 ? (size_t)p.NP : 1);
+  L.hist_s = take(sizeof(int32_t) * p.nbins * nch_s);
+  L.hist_p = take(sizeof(int32_t) * (nch_p ? p.nbins * nch_p : 1));
+  L.n_items = take(sizeof(int32_t) * 2);
+  L.order_p = take(sizeof(int32_t) * (p.NP > 0 ? p.NP : 1));
+  if (with_rowptr_col_order) {
+    L.row_ptr = take(sizeof(int32_t) * (p.R + 1));
+    L.col = take(sizeof(uint32_t) * (size_t)p.R * p.nKB);
+    L.order_s = take(sizeof(int32_t) * p.R);
+  }
+  L.total = off;
+  return L;
+}
+
+int stream_device(hipStream_t s, int* dev) {
+  hipError_t e = s ? hipStreamGetDevice(s, dev) : hipGetDevice(dev);
+  if (e != hipSuccess) return hip_fail(e, "querying the stream's device");
+  if (*dev < 0 || *dev >= kMaxDevices) return fail(STEEL_ERR_HIP, "device %d out of range", *dev);
+  return STEEL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* steel_version(void) { return "libsteel 0.1.0 (gfx950)"; }
+
+const char* steel_last_error(void) { return g_err.c_str(); }
+
+int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* block_mask,
+                   void* out, int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                   float scale, int causal, void* stream) {
+  g_err.clear();
+  if (!q || !k || !v || !out)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be non-NULL device pointers");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be 16-byte aligned");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "scale must be finite and > 0 (got %g)", (double)scale);
+  steel::Problem p{};
+  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  if (D != 64 && D != 128) return fail(STEEL_ERR_UNSUPPORTED, "D=%d not supported (64 or 128)", D);
+  p.D = D;
+  p.pack = (p.G % 4 == 0) ? 4 : (p.G % 2 == 0) ? 2 : 1;
+  p.NP = p.pack > 1 ? p.R / p.pack : 0;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
+  hipMemPool_t pool;
+  hipError_t e = device_pool(dev, &pool);
+  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
+  const Layout L = layout(p, true);
+  char* ws = nullptr;
+  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), L.total, pool, s);
+  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
+  steel::IndexBuffers w;
+  w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
+  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
+  w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
+  w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
+  w.row_ptr = reinterpret_cast<int32_t*>(ws + L.row_ptr);
+  w.col = reinterpret_cast<uint32_t*>(ws + L.col);
+  w.order_s = reinterpret_cast<int32_t*>(ws + L.order_s);
+  w.order_p = reinterpret_cast<int32_t*>(ws + L.order_p);
+  w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);
+  e = steel::launch_block_index(p, block_mask, w, s);
+  if (e == hipSuccess)
+    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), scale, w, s);
+  hipError_t ef = hipFreeAsync(ws, s);
+  if (e != hipSuccess) return hip_fail(e, "launching kernels");
+  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
+  return STEEL_OK;
+}
+
+int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k, int blk,
+                      int causal, int32_t* row_ptr, uint32_t* col, int32_t* order, void* stream) {
+  g_err.clear();
+  if (!row_ptr || !col || !order)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "row_ptr, col and order must be non-NULL");
+  steel::Problem p{};
+  int rc = check_shape(B, Hq, Hq, S_q, S_k, blk, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  p.D = 0;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
+  hipMemPool_t pool;
+  hipError_t e = device_pool(dev, &pool);
+  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
+  const Layout L = layout(p, false);
+  char* ws = nullptr;
+  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), L.total, pool, s);
+  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
+  steel::IndexBuffers w;
+  w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
+  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
+  w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
+  w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
+  w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);
+  w.order_p = reinterpret_cast<int32_t*>(ws + L.order_p);
+  w.row_ptr = row_ptr;
+  w.col = col;
+  w.order_s = order;
+  e = steel::launch_block_index(p, block_mask, w, s);
+  hipError_t ef = hipFreeAsync(ws, s);
+  if (e != hipSuccess) return hip_fail(e, "launching kernels");
+  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
+  return STEEL_OK;
+}
+
+}  // extern "C"

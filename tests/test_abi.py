@@ -1,0 +1,109 @@
+"""The C ABI on the CPU: the library builds, loads, exports every symbol the
+header declares, and rejects invalid arguments before any HIP call (no GPU
+needed: nothing is dereferenced or enqueued on those paths)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_09385_amd as steel
+from paper_2607_09385_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "steel.h")
+
+FAKE = 0x100000  # 16-byte aligned, never dereferenced on the checked paths
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(steel_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib.load()
+    names = declared_functions()
+    assert {"steel_attn_fwd", "steel_block_index", "steel_last_error", "steel_version"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), f"{name} declared in steel.h but not exported"
+
+
+def test_version_and_empty_error():
+    assert "gfx950" in steel.version()
+
+
+def attn(**kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, mask=None, out=FAKE, B=1, Hq=4, Hkv=2, S_q=128, S_k=128,
+                D=64, blk=64, scale=0.125, causal=1, stream=None)
+    args.update(kw)
+    lib = _lib.load()
+    st = lib.steel_attn_fwd(args["q"], args["k"], args["v"], args["mask"], args["out"],
+                            args["B"], args["Hq"], args["Hkv"], args["S_q"], args["S_k"],
+                            args["D"], args["blk"], args["scale"], args["causal"], args["stream"])
+    return st, _lib.last_error()
+
+
+@pytest.mark.parametrize("kw,code,text", [
+    (dict(q=None), 1, "non-NULL"),
+    (dict(out=None), 1, "non-NULL"),
+    (dict(k=FAKE + 8), 1, "aligned"),
+    (dict(out=FAKE + 4), 1, "aligned"),
+    (dict(Hq=3, Hkv=2), 1, "multiple"),
+    (dict(B=0), 1, ">= 1"),
+    (dict(S_q=0), 1, ">= 1"),
+    (dict(S_k=-5), 1, ">= 1"),
+    (dict(scale=float("nan")), 1, "scale"),
+    (dict(scale=float("inf")), 1, "scale"),
+    (dict(scale=0.0), 1, "scale"),
+    (dict(scale=-0.1), 1, "scale"),
+    (dict(causal=2), 1, "causal"),
+    (dict(D=96), 2, "D=96"),
+    (dict(D=256), 2, "D=256"),
+    (dict(blk=128), 2, "blk=128"),
+    (dict(B=1 << 20, Hq=1 << 10, Hkv=1, S_q=1 << 20), 2, "too large"),
+])
+def test_invalid_arguments_rejected(kw, code, text):
+    st, msg = attn(**kw)
+    assert st == code
+    assert text in msg
+
+
+def test_error_text_is_thread_local_and_cleared():
+    import threading
+    st, msg = attn(D=96)
+    assert st == 2 and "D=96" in msg
+    seen = []
+    t = threading.Thread(target=lambda: seen.append(_lib.last_error()))
+    t.start(); t.join()
+    assert seen == [""]
+    attn(Hq=3, Hkv=2)
+    assert "multiple" in _lib.last_error()
+
+
+def test_block_index_rejects_invalid():
+    lib = _lib.load()
+    st = lib.steel_block_index(None, 1, 1, 64, 64, 64, 1, None, FAKE, FAKE, None)
+    assert st == 1 and "non-NULL" in _lib.last_error()
+    st = lib.steel_block_index(None, 1, 1, 64, 64, 32, 1, FAKE, FAKE, FAKE, None)
+    assert st == 2 and "blk" in _lib.last_error()
+    st = lib.steel_block_index(None, 1, 1, 64, 0, 64, 1, FAKE, FAKE, FAKE, None)
+    assert st == 1
+
+
+def test_python_binding_checks(monkeypatch):
+    torch = pytest.importorskip("torch")
+    q = torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        steel.attn_fwd(q, q, q)
+    with pytest.raises(TypeError):
+        steel.attn_fwd(None, q, q)
+
+
+def test_valid_call_without_gpu_reports_hip_error():
+    torch = pytest.importorskip("torch")
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present; covered by the GPU tests")
+    st, msg = attn()
+    assert st == 3 and "HIP" in msg
