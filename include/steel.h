@@ -101,6 +101,36 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
                       int blk, int causal, int32_t* row_ptr, uint32_t* col,
                       int32_t* order, void* stream);
 
+/*
+ * Two-phase form of steel_attn_fwd for callers that reuse one mask over many
+ * calls (for example every layer of a model): steel_attn_plan builds the
+ * live-block index once into caller-owned device workspace, steel_attn_run
+ * runs the fused pass over it.  plan + run computes exactly what
+ * steel_attn_fwd computes.
+ *
+ *   steel_attn_workspace_bytes  size of the workspace for these sizes, or 0
+ *                               after an argument error (see
+ *                               steel_last_error())
+ *   workspace                   device memory, 256-byte aligned, at least
+ *                               that many bytes, owned by the caller; run
+ *                               only reads it, so several runs may share one
+ *                               plan concurrently
+ *
+ * run must be given the same B, Hq, Hkv, S_q, S_k, blk and causal as the plan
+ * (the kernels check a header the plan writes and leave out untouched on a
+ * mismatch), and must be ordered after the plan on the device (same stream,
+ * or an event).  Arguments mean what they mean for steel_attn_fwd.
+ */
+size_t steel_attn_workspace_bytes(int B, int Hq, int Hkv, int S_q, int S_k, int blk);
+
+int steel_attn_plan(const uint8_t* block_mask, int B, int Hq, int Hkv, int S_q, int S_k,
+                    int blk, int causal, void* workspace, size_t workspace_bytes, void* stream);
+
+int steel_attn_run(const void* q, const void* k, const void* v, void* out,
+                   int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                   float scale, int causal, const void* workspace, size_t workspace_bytes,
+                   void* stream);
+
 /* Text of the last non-OK status returned on the calling thread ("" if none). */
 const char* steel_last_error(void);
 

@@ -111,3 +111,53 @@ def block_index(block_mask, B: int, Hq: int, S_q: int, S_k: int, *, causal: bool
             _stream_handle(stream))
     _lib.check(st)
     return row_ptr, col, order
+
+
+class Plan:
+    """Live-block index built once for a mask and reused by ``run`` (the
+    two-phase form of ``attn_fwd``)."""
+
+    def __init__(self, block_mask, B: int, Hq: int, Hkv: int, S_q: int, S_k: int, *,
+                 causal: bool = True, blk: int = BLK, device=None, stream=None):
+        torch = _torch()
+        lib = _lib.load()
+        nbytes = lib.steel_attn_workspace_bytes(B, Hq, Hkv, S_q, S_k, blk)
+        if nbytes == 0:
+            raise SteelError(_lib.STEEL_ERR_INVALID_ARGUMENT, last_error())
+        if block_mask is not None:
+            nQB, nKB = -(-S_q // blk), -(-S_k // blk)
+            if block_mask.dtype != torch.uint8 or tuple(block_mask.shape) != (B, Hq, nQB, nKB):
+                raise ValueError("block_mask must be uint8 [B, Hq, nQB, nKB]")
+            if not block_mask.is_contiguous() or block_mask.device.type != "cuda":
+                raise ValueError("block_mask must be a contiguous GPU tensor")
+            device = block_mask.device
+        device = device or torch.device("cuda")
+        self.shape = (B, Hq, Hkv, S_q, S_k)
+        self.causal, self.blk, self.device = bool(causal), blk, device
+        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        with torch.cuda.device(device):
+            st = lib.steel_attn_plan(None if block_mask is None else block_mask.data_ptr(),
+                                     B, Hq, Hkv, S_q, S_k, blk, 1 if causal else 0,
+                                     self.workspace.data_ptr(), nbytes, _stream_handle(stream))
+        _lib.check(st)
+
+    def run(self, q, k, v, *, scale: Optional[float] = None, out=None, stream=None):
+        torch = _torch()
+        for name, t in (("q", q), ("k", k), ("v", v)):
+            _check_bf16(name, t)
+        B, Hq, Hkv, S_q, S_k = self.shape
+        D = q.shape[-1]
+        if tuple(q.shape) != (B, Hq, S_q, D) or tuple(k.shape) != (B, Hkv, S_k, D) \
+                or tuple(v.shape) != tuple(k.shape):
+            raise ValueError("q, k, v do not match the planned shape")
+        if scale is None:
+            scale = 1.0 / math.sqrt(D)
+        if out is None:
+            out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+        with torch.cuda.device(q.device):
+            st = _lib.load().steel_attn_run(
+                q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, Hq, Hkv, S_q, S_k,
+                D, self.blk, float(scale), 1 if self.causal else 0, self.workspace.data_ptr(),
+                self.workspace.numel(), _stream_handle(stream))
+        _lib.check(st)
+        return out

@@ -45,6 +45,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_block_index.restype = c_int
     lib.steel_block_index.argtypes = [c_void_p, c_int, c_int, c_int, c_int, c_int, c_int,
                                       c_void_p, c_void_p, c_void_p, c_void_p]
+    c_size_t = ctypes.c_size_t
+    lib.steel_attn_workspace_bytes.restype = c_size_t
+    lib.steel_attn_workspace_bytes.argtypes = [c_int] * 6
+    lib.steel_attn_plan.restype = c_int
+    lib.steel_attn_plan.argtypes = [c_void_p] + [c_int] * 7 + [c_void_p, c_size_t, c_void_p]
+    lib.steel_attn_run.restype = c_int
+    lib.steel_attn_run.argtypes = [c_void_p] * 4 + [c_int] * 7 + [c_float, c_int, c_void_p,
+                                                                  c_size_t, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

@@ -47,8 +47,9 @@ struct AttnArgs {
   const int32_t* row_ptr;
   const uint32_t* col;
   const int32_t* order;
-  const int32_t* n_items;
-  int Hq, Hkv, S_q, S_k, nQB, G, causal, delta;
+  const int32_t* n_items;   // this list's item count
+  const int32_t* header;    // plan header (after the two counts)
+  int Hq, Hkv, S_q, S_k, nQB, nKB, G, causal, delta, R, pack;
   float c;  // scale * log2(e)
 };
 
@@ -75,6 +76,10 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) __bf16 sK[kBlk * ST];
   __shared__ __attribute__((aligned(16))) __bf16 sV[kBlk * ST];
 
+  const int32_t* hd = a.header;
+  if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
+      hd[4] != a.causal || hd[5] != a.delta)
+    return;  // index was planned for another problem: leave out untouched
   if ((int)blockIdx.x >= a.n_items[0]) return;
   const int item = a.order[blockIdx.x];
   const int qb = item % a.nQB;
@@ -247,6 +252,10 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.col = w.col;
   a.order = nullptr;
   a.n_items = nullptr;
+  a.header = w.n_items + 2;
+  a.nKB = p.nKB;
+  a.R = p.R;
+  a.pack = p.pack;
   a.Hq = p.Hq;
   a.Hkv = p.Hkv;
   a.S_q = p.S_q;

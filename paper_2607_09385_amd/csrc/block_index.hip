@@ -141,6 +141,12 @@ __global__ __launch_bounds__(1024) void k_scan(Problem p, const int32_t* __restr
   if (threadIdx.x == 0) {
     n_items[0] = ns;
     n_items[1] = np;
+    n_items[2] = kPlanMagic;
+    n_items[3] = p.R;
+    n_items[4] = p.nKB;
+    n_items[5] = p.pack;
+    n_items[6] = p.causal;
+    n_items[7] = p.delta;
   }
 }
 

@@ -34,8 +34,13 @@ struct IndexBuffers {
   uint32_t* col;       // [R*nKB] capacity
   int32_t* order_s;    // [R]   single-head items, heaviest first
   int32_t* order_p;    // [NP]  head-pack items, heaviest first
-  int32_t* n_items;    // [2]   {single, pack} item counts
+  int32_t* n_items;    // [8]   {single items, pack items, plan header ...}
 };
+
+// Plan header written after the two item counts; the attention kernels check
+// it against their own arguments before touching the index.
+constexpr int kPlanMagic = 0x5354454c;  // "STEL"
+constexpr int kHeaderInts = 8;
 
 inline int nchunks(int n) { return (n + kChunk - 1) / kChunk; }
 

@@ -123,7 +123,7 @@ Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
   L.uni = take(p.NP > 0 ? (size_t)p.NP : 1);
   L.hist_s = take(sizeof(int32_t) * p.nbins * nch_s);
   L.hist_p = take(sizeof(int32_t) * (nch_p ? p.nbins * nch_p : 1));
-  L.n_items = take(sizeof(int32_t) * 2);
+  L.n_items = take(sizeof(int32_t) * steel::kHeaderInts);
   L.order_p = take(sizeof(int32_t) * (p.NP > 0 ? p.NP : 1));
   if (with_rowptr_col_order) {
     L.row_ptr = take(sizeof(int32_t) * (p.R + 1));
@@ -141,6 +141,54 @@ int stream_device(hipStream_t s, int* dev) {
   return STEEL_OK;
 }
 
+// Argument checks of the fused pass (everything but the workspace).
+int check_attn(const void* q, const void* k, const void* v, const void* out, int B, int Hq,
+               int Hkv, int S_q, int S_k, int D, int blk, float scale, int causal,
+               steel::Problem* p) {
+  if (!q || !k || !v || !out)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be non-NULL device pointers");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be 16-byte aligned");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "scale must be finite and > 0 (got %g)", (double)scale);
+  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, p);
+  if (rc != STEEL_OK) return rc;
+  if (D != 64 && D != 128) return fail(STEEL_ERR_UNSUPPORTED, "D=%d not supported (64 or 128)", D);
+  p->D = D;
+  return STEEL_OK;
+}
+
+// Head packing: query heads of one key/value group that share a live list run
+// in one workgroup (up to 4).
+void set_pack(steel::Problem* p) {
+  p->pack = (p->G % 4 == 0) ? 4 : (p->G % 2 == 0) ? 2 : 1;
+  p->NP = p->pack > 1 ? p->R / p->pack : 0;
+}
+
+steel::IndexBuffers carve(char* ws, const Layout& L) {
+  steel::IndexBuffers w;
+  w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
+  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
+  w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
+  w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
+  w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);
+  w.order_p = reinterpret_cast<int32_t*>(ws + L.order_p);
+  w.row_ptr = reinterpret_cast<int32_t*>(ws + L.row_ptr);
+  w.col = reinterpret_cast<uint32_t*>(ws + L.col);
+  w.order_s = reinterpret_cast<int32_t*>(ws + L.order_s);
+  return w;
+}
+
+int check_workspace(const void* ws, size_t bytes, const Layout& L) {
+  if (!ws) return fail(STEEL_ERR_INVALID_ARGUMENT, "workspace must be a non-NULL device pointer");
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "workspace must be 256-byte aligned");
+  if (bytes < L.total)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "workspace of %zu bytes is smaller than the %zu needed",
+                bytes, L.total);
+  return STEEL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -153,19 +201,10 @@ int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* b
                    void* out, int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
                    float scale, int causal, void* stream) {
   g_err.clear();
-  if (!q || !k || !v || !out)
-    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be non-NULL device pointers");
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out))
-    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k, v and out must be 16-byte aligned");
-  if (!std::isfinite(scale) || !(scale > 0.f))
-    return fail(STEEL_ERR_INVALID_ARGUMENT, "scale must be finite and > 0 (got %g)", (double)scale);
   steel::Problem p{};
-  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, &p);
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
   if (rc != STEEL_OK) return rc;
-  if (D != 64 && D != 128) return fail(STEEL_ERR_UNSUPPORTED, "D=%d not supported (64 or 128)", D);
-  p.D = D;
-  p.pack = (p.G % 4 == 0) ? 4 : (p.G % 2 == 0) ? 2 : 1;
-  p.NP = p.pack > 1 ? p.R / p.pack : 0;
+  set_pack(&p);
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
@@ -177,22 +216,54 @@ int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* b
   char* ws = nullptr;
   e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), L.total, pool, s);
   if (e != hipSuccess) return hip_fail(e, "allocating workspace");
-  steel::IndexBuffers w;
-  w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
-  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
-  w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
-  w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
-  w.row_ptr = reinterpret_cast<int32_t*>(ws + L.row_ptr);
-  w.col = reinterpret_cast<uint32_t*>(ws + L.col);
-  w.order_s = reinterpret_cast<int32_t*>(ws + L.order_s);
-  w.order_p = reinterpret_cast<int32_t*>(ws + L.order_p);
-  w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);
+  const steel::IndexBuffers w = carve(ws, L);
   e = steel::launch_block_index(p, block_mask, w, s);
   if (e == hipSuccess)
     e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), scale, w, s);
   hipError_t ef = hipFreeAsync(ws, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
+  return STEEL_OK;
+}
+
+size_t steel_attn_workspace_bytes(int B, int Hq, int Hkv, int S_q, int S_k, int blk) {
+  g_err.clear();
+  steel::Problem p{};
+  if (check_shape(B, Hq, Hkv, S_q, S_k, blk, 0, &p) != STEEL_OK) return 0;
+  set_pack(&p);
+  return layout(p, true).total;
+}
+
+int steel_attn_plan(const uint8_t* block_mask, int B, int Hq, int Hkv, int S_q, int S_k,
+                    int blk, int causal, void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  set_pack(&p);
+  const Layout L = layout(p, true);
+  if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
+  hipError_t e = steel::launch_block_index(p, block_mask, carve(static_cast<char*>(workspace), L),
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "launching the index build");
+  return STEEL_OK;
+}
+
+int steel_attn_run(const void* q, const void* k, const void* v, void* out, int B, int Hq,
+                   int Hkv, int S_q, int S_k, int D, int blk, float scale, int causal,
+                   const void* workspace, size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  set_pack(&p);
+  const Layout L = layout(p, true);
+  if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
+  hipError_t e = steel::launch_attention(
+      p, q, k, v, static_cast<float*>(out), scale,
+      carve(const_cast<char*>(static_cast<const char*>(workspace)), L),
+      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "launching the attention kernels");
   return STEEL_OK;
 }
 

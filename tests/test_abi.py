@@ -107,3 +107,25 @@ def test_valid_call_without_gpu_reports_hip_error():
         pytest.skip("a GPU is present; covered by the GPU tests")
     st, msg = attn()
     assert st == 3 and "HIP" in msg
+
+
+def test_workspace_bytes_and_plan_run_checks():
+    lib = _lib.load()
+    n = lib.steel_attn_workspace_bytes(1, 32, 8, 16384, 16384, 64)
+    assert n > 256 * 256 * 8 * 4            # holds at least the live list capacity
+    assert lib.steel_attn_workspace_bytes(1, 3, 2, 64, 64, 64) == 0
+    assert "multiple" in _lib.last_error()
+    # plan: NULL / misaligned / short workspace, all before any HIP call
+    st = lib.steel_attn_plan(None, 1, 4, 2, 128, 128, 64, 1, None, n, None)
+    assert st == 1 and "workspace" in _lib.last_error()
+    st = lib.steel_attn_plan(None, 1, 4, 2, 128, 128, 64, 1, FAKE + 16, n, None)
+    assert st == 1 and "256-byte" in _lib.last_error()
+    need = lib.steel_attn_workspace_bytes(1, 4, 2, 128, 128, 64)
+    st = lib.steel_attn_plan(None, 1, 4, 2, 128, 128, 64, 1, FAKE, need - 1, None)
+    assert st == 1 and "smaller" in _lib.last_error()
+    st = lib.steel_attn_run(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 96, 64, 0.1, 1, FAKE, need,
+                            None)
+    assert st == 2 and "D=96" in _lib.last_error()
+    st = lib.steel_attn_run(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.1, 1, FAKE, 16,
+                            None)
+    assert st == 1 and "smaller" in _lib.last_error()

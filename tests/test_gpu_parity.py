@@ -210,3 +210,25 @@ def test_overwrites_output_buffer():
     s.attn_fwd(q.to(dev), k.to(dev), v.to(dev), torch.from_numpy(m).to(dev), causal=True, out=out)
     torch.cuda.synchronize()
     assert torch.all(out == 0).item()
+
+
+def test_plan_run_equals_fused_call_and_rejects_mismatch():
+    say("[parity] plan + run == attn_fwd; mismatched plan leaves out untouched")
+    s = steel()
+    dev = torch.device("cuda:0")
+    q, k, v = small_qkv(9, 1, 8, 2, 640, 640, 128)
+    m = random_block_mask(np.random.default_rng(9), 1, 8, 10, 10, p=0.5)
+    qd, kd, vd, md = q.to(dev), k.to(dev), v.to(dev), torch.from_numpy(m).to(dev)
+    a = s.attn_fwd(qd, kd, vd, md, causal=True)
+    plan = s.Plan(md, 1, 8, 2, 640, 640, causal=True, device=dev)
+    b1 = plan.run(qd, kd, vd)
+    b2 = plan.run(qd, kd, vd)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b1) and torch.equal(a, b2)
+    # a plan for the non-causal problem run as causal: header mismatch, out untouched
+    plan_nc = s.Plan(md, 1, 8, 2, 640, 640, causal=False, device=dev)
+    plan_nc.causal = True
+    out = torch.full((1, 8, 640, 128), 7.0, device=dev)
+    plan_nc.run(qd, kd, vd, out=out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0).item()
