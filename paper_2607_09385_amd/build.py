@@ -27,6 +27,9 @@ COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
+    # keep MFMA accumulators in VGPRs: the softmax reads the scores with VALU
+    # instructions, and AGPR-resident accumulators cost a copy per element
+    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
 
 

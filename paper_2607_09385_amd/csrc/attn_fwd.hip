@@ -27,7 +27,16 @@
 // (2 waves, 64 rows) or a pack of PACK query heads of one key/value group
 // that share the same live list (2*PACK waves), so each K/V tile is loaded
 // once for up to 256 query rows.
+#include <climits>
+
 #include "internal.h"
+
+#ifndef STEEL_NT
+#define STEEL_NT 1
+#endif
+#ifndef STEEL_STAGES
+#define STEEL_STAGES 4
+#endif
 
 namespace steel {
 
@@ -66,22 +75,104 @@ __device__ __forceinline__ float half_pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-template <int D, int PACK>
-__global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
-  constexpr int NT = 128 * PACK;   // threads
-  constexpr int ST = D + 8;        // LDS row stride (bf16): 16-byte pad
+// LDS tile layout: 64 rows (keys) x D bf16, no padding, 16-byte chunks
+// XOR-swizzled within a row: chunk c of row r sits at chunk slot
+// c ^ swz(r).  swz is linear over the row bits it reads (D = 128: bits 0-3;
+// D = 64: bits 1-3), which makes both the 16-byte K reads (32 consecutive
+// rows, same chunk) and the transposed V reads (4 rows x 4 chunks per
+// 32 lanes) free of LDS bank conflicts on 64 banks, and lets every lane keep
+// its read offsets in a few registers.
+template <int D>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+}
+
+template <int D>
+__device__ __forceinline__ int tile_elem(int r, int c) {  // bf16 offset of (row, chunk)
+  return (r * (D / 8) + (c ^ swz<D>(r))) * 8;
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone: waits until at most
+// N of this wave's vector memory operations (here: global -> LDS copies) are
+// still in flight.  vmcnt is split over bits [3:0] and [15:14].
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void glob_void;
+
+// One 16-byte global -> LDS copy per lane (global_load_lds_dwordx4, SGPR
+// base + 32-bit VGPR offset): lane i writes LDS bytes
+// [lds_base + 16 i, lds_base + 16 i + 16).  Issued as inline assembly so the
+// compiler does not treat every later LDS read as possibly aliasing the copy
+// (it would insert a full vmcnt wait before each one); the kernel itself
+// waits (wait_vm) and barriers before any wave reads the data.
+__device__ __forceinline__ void copy16_to_lds(const void* sbase, uint32_t voff, uint32_t lds_base) {
+  // the base pointer and the LDS address are wave-uniform: keep them in SGPRs
+  // (readfirstlane returns int: widen through uint32_t so the low half is not
+  // sign-extended into the high half)
+  const uint64_t p = (uint64_t)(uintptr_t)sbase;
+  const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint64_t ps = (hi << 32) | lo;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(ps)
+               : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+typedef const __attribute__((address_space(4))) int32_t* cint_p;
+typedef const __attribute__((address_space(4))) uint32_t* cuint_p;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+template <int P> struct Par { static constexpr int value = P; };
+
+// Depth of the K/V ring (stages of one K tile and one V tile each).
+template <int D, int PACK, int NT>
+constexpr int stages_for() { return STEEL_STAGES; }
+
+// Rows per wave: 32 (NT = 1), so that two waves share each SIMD and one can
+// issue MFMAs while the other computes exponentials.
+template <int D>
+constexpr int nt_for() { return STEEL_NT; }
+
+
+// Workgroup = PACK heads x 64 query rows.  Each wave owns NT 32-row MFMA
+// N-tiles of one head: NT = 2 (one wave per head; every K/V fragment read from
+// LDS feeds two MFMAs; the wave needs most of the register file) or NT = 1
+// (two waves per head, half the registers, so two waves share a SIMD).
+template <int D, int PACK, int NT>
+__global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
+  constexpr int WPH = 2 / NT;      // waves per head
+  constexpr int NW = PACK * WPH;   // waves
+  constexpr int C = D / 8;         // 16-byte chunks per row
+  constexpr int TE = kBlk * D;     // bf16 elements per tile
+  constexpr int TB = TE * 2;       // bytes per tile
+  constexpr int LPW = C / NW;      // 16-byte copies per lane per tile (per tensor)
   constexpr int KS = D / 16;       // k-steps of S^T = K Q^T
   constexpr int DT = D / 32;       // d tiles of O^T
-  constexpr int CH = kBlk * D / 8; // 16-byte chunks per tile
-  __shared__ __attribute__((aligned(16))) __bf16 sK[kBlk * ST];
-  __shared__ __attribute__((aligned(16))) __bf16 sV[kBlk * ST];
+  constexpr float TAU = 8.0f;      // rescale only when the row max grows by > 2^8
+  static_assert(LPW >= 1 && C % NW == 0, "tile copy split");
+  // A ring of ST stages, each holding the K and the V tile of one key block:
+  // tiles i+1 .. i+ST-1 are being copied in while tile i is computed on.
+  constexpr int ST = stages_for<D, PACK, NT>();
+  __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
 
-  const int32_t* hd = a.header;
+  // index data is read-only during the kernel: scalar loads
+  const cint_p hd = (cint_p)a.header;
   if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
       hd[4] != a.causal || hd[5] != a.delta)
     return;  // index was planned for another problem: leave out untouched
-  if ((int)blockIdx.x >= a.n_items[0]) return;
-  const int item = a.order[blockIdx.x];
+  if ((int)blockIdx.x >= ((cint_p)a.n_items)[0]) return;
+  const int item = ((cint_p)a.order)[blockIdx.x];
   const int qb = item % a.nQB;
   const int bh0 = (item / a.nQB) * PACK;  // b*Hq + first head
   const int b = bh0 / a.Hq;
@@ -89,142 +180,327 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
   const int g = h0 / a.G;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int head = h0 + (wave >> 1);
+  const int head = h0 + wave / WPH;
   const int n = lane & 31, hf = lane >> 5;
-  const int qrow = qb * kBlk + (wave & 1) * 32 + n;
-
-  // Q rows as the B operand: lane holds row n, d = 16*ks + 8*hf + 0..7
-  bf16x8 qf[KS];
-  {
-    const __bf16* qp = a.q + (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 8 * hf;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (qrow < a.S_q) qf[ks] = *(const bf16x8*)(qp + 16 * ks);
-      else qf[ks] = bf16x8{};
-    }
-  }
-
-  f32x16 o[DT];
-#pragma unroll
-  for (int t = 0; t < DT; ++t) o[t] = f32x16{};
-  float m = -INFINITY, l = 0.f;
+  const int qrow0 = qb * kBlk + (wave % WPH) * 32 + n;  // N-tile nt holds row qrow0 + 32*nt
 
   const int r0 = bh0 * a.nQB + qb;
-  const int beg = a.row_ptr[r0], end = a.row_ptr[r0 + 1];
+  const int beg = ((cint_p)a.row_ptr)[r0];
+  const int L = ((cint_p)a.row_ptr)[r0 + 1] - beg;
+  const cuint_p colp = (cuint_p)a.col + beg;
   const size_t kvoff = ((size_t)b * a.Hkv + g) * a.S_k * D;
   const __bf16* kg = a.k + kvoff;
   const __bf16* vg = a.v + kvoff;
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
 
-  // lane constants of the transposed V read (16-lane groups)
+  // copy plan: copy j of this lane fills tile slot (wave*LPW + j)*64 + lane,
+  // i.e. row r = slot / C, chunk slot % C, which holds source chunk
+  // (slot % C) ^ swz(r) of key row r.
+  uint32_t cp_off[LPW];
+  int cp_row[LPW];
+#pragma unroll
+  for (int j = 0; j < LPW; ++j) {
+    const int slot = (wave * LPW + j) * 64 + lane;
+    const int r = slot / C;
+    cp_row[j] = r;
+    cp_off[j] = (uint32_t)((r * D + ((slot % C) ^ swz<D>(r)) * 8) * 2);
+  }
+  // Copy key block kb of K (or V) into the tile buffer at LDS byte offset
+  // dst.  Rows past S_k (the tail block) read the last key row instead.
+  auto issue_copy = [&](const __bf16* src, uint32_t dst, int kb) {
+    const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW) * 1024u;
+    if ((kb + 1) * kBlk <= a.S_k) {
+      const __bf16* sb = src + (size_t)kb * kBlk * D;
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) copy16_to_lds(sb, cp_off[j], lbase + j * 1024u);
+    } else {
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) {
+        const int key = min(kb * kBlk + cp_row[j], a.S_k - 1);
+        const uint32_t off = cp_off[j] + (uint32_t)((key - cp_row[j]) * D * 2);
+        copy16_to_lds(src, off, lbase + j * 1024u);
+      }
+    }
+  };
+
+  // Per-lane LDS read offsets in bytes (tile buffer base and the row block of
+  // each fragment are compile-time immediates):
+  //   K fragment (sg, ks): row 32*sg + n, chunk (2*ks + hf)
+  //   V fragment (sg, t, cc, dt): row 32*sg + 16*t + 8*cc + 4*(tg>>1) + tr,
+  //                               chunk 4*dt + 2*(tg&1) + (tq>>1), half tq&1
+  uint32_t koff[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = (uint32_t)tile_elem<D>(n, 2 * ks + hf) * 2;
   const int tg = lane >> 4, tr = (lane >> 2) & 3, tq = lane & 3;
-  const int v_lane_off = (4 * (tg >> 1) + tr) * ST + 16 * (tg & 1) + 4 * tq;
-  const int k_lane_off = n * ST + 8 * hf;
+  uint32_t voff[2][DT];
+#pragma unroll
+  for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int row = 8 * cc + 4 * (tg >> 1) + tr;
+      voff[cc][dt] = (uint32_t)(tile_elem<D>(row, 4 * dt + 2 * (tg & 1) + (tq >> 1)) + 4 * (tq & 1)) * 2;
+    }
 
-  for (int it = beg; it < end; ++it) {
-    const uint32_t cw = a.col[it];
+  // Prologue.  Tile 0 is copied in while Q is fetched; the Q fragments are
+  // then consumed by an empty asm statement, which makes the compiler wait for
+  // its Q loads here, before the loop (and with them for tile 0, issued
+  // earlier).  Left to itself it would put that wait at the first use inside
+  // the loop, where it would drain every in-flight copy on each iteration.
+  // Only then are tiles 1 .. ST-2 put in flight.  Stage s holds K at byte
+  // offset 2*s*TB and V at (2*s + 1)*TB.
+  constexpr int CPT = 2 * LPW;  // copy instructions per lane per tile
+  if (L > 0) {
+    const int kb = (int)(colp[0] & 0x7fffffffu);
+    issue_copy(kg, 0, kb);
+    issue_copy(vg, TB, kb);
+  }
+
+  // Q rows as the B operand: N-tile nt, lane holds row 32*nt + n, d = 16*ks + 8*hf + 0..7
+  bf16x8 qf[NT][KS];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const __bf16* qp =
+        a.q + (((size_t)b * a.Hq + head) * a.S_q + min(qrow0 + 32 * nt, a.S_q - 1)) * D + 8 * hf;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qp + 16 * ks);
+  }
+  // The live list is kept in two VGPRs (entries 64j .. 64j+127, one per
+  // lane) and entries are extracted with v_readlane.  Scalar loads inside the
+  // loop would make every LDS wait an lgkmcnt(0) wait for them.
+  const uint32_t* colv = a.col + beg;
+  auto load_win = [&](int base) -> uint32_t {
+    return base + lane < L ? colv[base + lane] : 0u;
+  };
+  int wbase = 0;
+  uint32_t win0 = load_win(0), win1 = load_win(64);
+  auto entry = [&](int k) -> uint32_t {  // k in [wbase, wbase + 128)
+    const int off = k - wbase;
+    return (uint32_t)__builtin_amdgcn_readlane((int)(off < 64 ? win0 : win1), off & 63);
+  };
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qf[nt][ks]));
+  asm volatile("" ::"v"(win0), "v"(win1));
+  wait_vm<0>();
+
+#pragma unroll
+  for (int s = 1; s < ST - 1; ++s)
+    if (s < L) {
+      const int kb = (int)(colp[s] & 0x7fffffffu);
+      issue_copy(kg, (2 * s) * TB, kb);
+      issue_copy(vg, (2 * s + 1) * TB, kb);
+    }
+
+  f32x16 o[NT][DT];
+  float m[NT], l[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+    for (int t = 0; t < DT; ++t) o[nt][t] = f32x16{};
+    m[nt] = -INFINITY;
+    l[nt] = 0.f;
+  }
+
+  const char* lds_bytes = (const char*)smem;
+  auto ld_k = [&](int S, int sg, int ks) -> bf16x8 {
+    return *(const bf16x8*)(lds_bytes + 2 * S * TB + sg * 32 * D * 2 + koff[ks]);
+  };
+  auto ld_v = [&](int S, int sg, int t, int dt) -> bf16x8 {
+    const char* base = lds_bytes + (2 * S + 1) * TB + (32 * sg + 16 * t) * D * 2;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[0][dt]));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[1][dt]));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+
+  // tile 0 has landed (waited for with Q); make it visible to every wave
+  if (L > 0) __syncthreads();
+
+  // One iteration for tile i.  S = i % ST is a compile-time constant (the
+  // loop is unrolled ST times), so every LDS offset folds into an
+  // instruction immediate.
+  auto step = [&](int i, auto stage) {
+    constexpr int S = decltype(stage)::value;
+    // slide the list window when entry i + ST - 1 would leave it (once per
+    // 64 tiles; the load is waited for at once)
+    if (i + ST - 1 >= wbase + 128) {
+      wbase += 64;
+      win0 = win1;
+      win1 = load_win(wbase + 64);
+      asm volatile("" ::"v"(win1));
+    }
+    const uint32_t cw = entry(i);
     const int kb = (int)(cw & 0x7fffffffu);
     const bool partial = (cw >> 31) != 0;
-
-    __syncthreads();  // previous tile fully consumed
-#pragma unroll
-    for (int c = tid; c < CH; c += NT) {
-      const int row = c / (D / 8), c8 = c % (D / 8);
-      const int key = kb * kBlk + row;
-      u32x4 kk = u32x4{0, 0, 0, 0}, vv = u32x4{0, 0, 0, 0};
-      if (key < a.S_k) {
-        kk = *(const u32x4*)(kg + (size_t)key * D + c8 * 8);
-        vv = *(const u32x4*)(vg + (size_t)key * D + c8 * 8);
-      }
-      *(u32x4*)(sK + row * ST + c8 * 8) = kk;
-      *(u32x4*)(sV + row * ST + c8 * 8) = vv;
+    // refill the stage tile i-1 used (free since the barrier that ended it)
+    const bool refill = i + ST - 1 < L;
+    if (refill) {
+      constexpr int SN = (S + ST - 1) % ST;
+      const int kbn = (int)(entry(i + ST - 1) & 0x7fffffffu);
+      issue_copy(kg, (2 * SN) * TB, kbn);
+      issue_copy(vg, (2 * SN + 1) * TB, kbn);
     }
-    __syncthreads();
 
-    // S^T = K Q^T for two 32-key sub-tiles
-    f32x16 s[2];
-#pragma unroll
-    for (int sg = 0; sg < 2; ++sg) {
-      s[sg] = f32x16{};
+    // S^T = K Q^T; K fragments read one step ahead of their MFMAs
+    f32x16 sc[NT][2];
+    {
+      bf16x8 kf[2][2];
+      kf[0][0] = ld_k(S, 0, 0);
+      kf[0][1] = ld_k(S, 1, 0);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        const bf16x8 ka = *(const bf16x8*)(sK + k_lane_off + sg * 32 * ST + 16 * ks);
-        s[sg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], s[sg], 0, 0, 0);
+        const int cb = ks & 1;
+        if (ks + 1 < KS) {
+          kf[cb ^ 1][0] = ld_k(S, 0, ks + 1);
+          kf[cb ^ 1][1] = ld_k(S, 1, ks + 1);
+        }
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt) {
+            if (ks == 0) sc[nt][sg] = f32x16{};
+            sc[nt][sg] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[cb][sg], qf[nt][ks], sc[nt][sg], 0, 0, 0);
+          }
       }
     }
 
     if (partial) {
+      // Element mask from coordinates (Section IV-A case iii): key j of the
+      // tile is visible to row i iff j <= i + delta (causal) and j < S_k.
+      // One threshold per row; each element is kept or set to -inf with an
+      // arithmetic select (no per-element condition registers).
 #pragma unroll
-      for (int sg = 0; sg < 2; ++sg)
+      for (int nt = 0; nt < NT; ++nt) {
+        const int lim_abs = min(a.causal ? qrow0 + 32 * nt + a.delta : INT_MAX - kBlk, a.S_k - 1);
+        const int lim = lim_abs - (kb * kBlk + 4 * hf);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kb * kBlk + 32 * sg + 8 * (r >> 2) + 4 * hf + (r & 3);
-          const bool vis = key < a.S_k && (!a.causal || key <= qrow + a.delta);
-          if (!vis) s[sg][r] = -INFINITY;
-        }
+        for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int off = 32 * sg + 8 * (r >> 2) + (r & 3);
+            const unsigned dead = (unsigned)((lim - off) >> 31);  // all ones if off > lim
+            sc[nt][sg][r] = __uint_as_float((dead & 0xff800000u) |
+                                            (~dead & __float_as_uint(sc[nt][sg][r])));
+          }
+      }
     }
 
-    float mx = -INFINITY;
+    float mt[NT];
+    bool grow = false;
 #pragma unroll
-    for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[sg][r]);
-    mx = other_half_max(mx);
-    const float mt = mx == -INFINITY ? -INFINITY : mx * a.c;
-    const float mnew = fmaxf(m, mt);
-    const float msafe = mnew == -INFINITY ? 0.f : mnew;
-    const float alpha = __builtin_amdgcn_exp2f(m - msafe);
-
-    float rs = 0.f;
-    bf16x8 pb[2][2];
-#pragma unroll
-    for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(s[sg][8 * t + e], a.c, -msafe));
-          rs += pv;
-          pb[sg][t][e] = (__bf16)pv;
-        }
-    l = alpha * l + rs;
-    m = mnew;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-
-    // O^T += V^T P^T
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+    for (int nt = 0; nt < NT; ++nt) {
+      float mx = -INFINITY;
 #pragma unroll
       for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const __bf16* base = sV + v_lane_off + (32 * sg + 16 * t) * ST + 32 * dt;
-          const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base));
-          const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + 8 * ST));
-          const s16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-          o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, both),
-                                                          pb[sg][t], o[dt], 0, 0, 0);
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[nt][sg][r]);
+      mx = other_half_max(mx);
+      mt[nt] = mx == -INFINITY ? -INFINITY : mx * a.c;
+      grow |= mt[nt] > m[nt] + TAU;
+    }
+    // Rescale only when some row's maximum grew by more than TAU (log2
+    // units): P = 2^(S - m) then stays below 2^TAU, and m cancels in O / l.
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const float mnew = fmaxf(m[nt], mt[nt]);
+        const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
+        l[nt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[nt][dt] *= alpha;
+        m[nt] = mnew;
+      }
+    }
+    float msafe[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
+
+    // P.V in four phases, one per 16-key chunk k = (sg, t): phase k runs the
+    // MFMAs of chunk k while the exponentials of chunk k+1 are computed and
+    // the V fragments of chunk k+1 are read.  The row sums add the
+    // bf16-rounded P that the MFMAs consume (v_dot2 against (1, 1)), so
+    // O / l weights the value rows exactly as used.
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    auto exps = [&](int k, bf16x8* p) {
+      const int sg = k >> 1, t = k & 1;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          p[nt][e] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(sc[nt][sg][8 * t + e], a.c, -msafe[nt]));
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          l[nt] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{p[nt][e], p[nt][e + 1]}, ones, l[nt], false);
+      }
+    };
+    bf16x8 vf[2][DT], pa[2][NT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[0][dt] = ld_v(S, 0, 0, dt);
+    exps(0, pa[0]);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int cur = k & 1, nx = cur ^ 1;
+      if (k < 3) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) vf[nx][dt] = ld_v(S, (k + 1) >> 1, (k + 1) & 1, dt);
+        exps(k + 1, pa[nx]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          o[nt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[cur][dt], pa[cur][nt], o[nt][dt], 0, 0, 0);
+    }
+
+    // tile i+1 must have landed before the barrier: newer copies (tiles
+    // i+2 .. i+ST-1, CPT instructions each) may stay in flight
+    if (i + 1 < L) {
+      if (i + ST - 1 < L) wait_vm<(ST - 2) * CPT>();
+      else wait_vm<0>();
+    }
+    __syncthreads();  // tile i's stage may be refilled from here on
+  };
+
+  int i = 0;
+  for (; i + ST <= L; i += ST) {
+#pragma unroll
+    for (int u = 0; u < ST; ++u) {
+      if (u == 0) step(i, Par<0>{});
+      if (u == 1) step(i + 1, Par<(1 % ST)>{});
+      if (u == 2 && ST > 2) step(i + 2, Par<(2 % ST)>{});
+      if (u == 3 && ST > 3) step(i + 3, Par<(3 % ST)>{});
+    }
+  }
+  for (int u = 0; i < L; ++i, ++u) {
+    if (u == 0) step(i, Par<0>{});
+    else if (u == 1) step(i, Par<(1 % ST)>{});
+    else if (u == 2) step(i, Par<(2 % ST)>{});
   }
 
-  const float lt = half_pair_sum(l);
-  const float inv = lt > 0.f ? 1.f / lt : 0.f;
-  if (qrow < a.S_q) {
-    float* op = a.out + (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+  for (int nt = 0; nt < NT; ++nt) {
+    const int qrow = qrow0 + 32 * nt;
+    const float lt = half_pair_sum(l[nt]);
+    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    if (qrow < a.S_q) {
+      float* op = a.out + (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
-        f32x4 w = {o[dt][4 * gq] * inv, o[dt][4 * gq + 1] * inv, o[dt][4 * gq + 2] * inv,
-                   o[dt][4 * gq + 3] * inv};
-        *(f32x4*)(op + 32 * dt + 8 * gq) = w;
-      }
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+          f32x4 w = {o[nt][dt][4 * gq] * inv, o[nt][dt][4 * gq + 1] * inv,
+                     o[nt][dt][4 * gq + 2] * inv, o[nt][dt][4 * gq + 3] * inv};
+          *(f32x4*)(op + 32 * dt + 8 * gq) = w;
+        }
+    }
   }
 }
 
 template <int D, int PACK>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
-  if (grid > 0) hipLaunchKernelGGL((k_attn<D, PACK>), dim3(grid), dim3(128 * PACK), 0, s, a);
+  constexpr int NT = nt_for<D>();
+  if (grid > 0)
+    hipLaunchKernelGGL((k_attn<D, PACK, NT>), dim3(grid), dim3(64 * PACK * (2 / NT)), 0, s, a);
 }
 
 template <int D>
