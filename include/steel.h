@@ -89,10 +89,11 @@ int steel_attn_fwd(const void* q, const void* k, const void* v,
  *            row_ptr[r] .. row_ptr[r+1]-1 hold the live kb in increasing
  *            order, bit 31 set for a partial block.  Capacity must be at
  *            least R*nKB (the live total is only known on the device).
- *   order    int32 [R], device: the rows sorted by live count, heaviest
- *            first, equal counts in increasing row order.  When nKB >= 4096
- *            the count is first divided by the smallest power of two that
- *            brings it below 4096.
+ *   order    int32 [R], device: the rows sorted by the bin of their live
+ *            count, heaviest first, equal bins in increasing row order.  The
+ *            bin of a count c is c itself when c < 128; above, with
+ *            e = floor(log2 c), it is 128 + 16*(e - 7) + ((c >> (e - 4)) & 15)
+ *            (16 bins per octave, all bins below 512).
  *
  * The arguments shared with steel_attn_fwd mean the same and are checked the
  * same way; D and the tensors are not needed here.

@@ -19,4 +19,4 @@ force on tiny inputs, closed forms, invariants and an independent library
 routine (see the module docstrings).
 """
 from .masked_attention import attention, attention_rows, element_visibility, kv_head  # noqa: F401
-from .block_index import build_index, tile_classes, work_order  # noqa: F401
+from .block_index import N_BINS, build_index, count_bin, tile_classes, work_order  # noqa: F401

@@ -26,6 +26,9 @@ order, with bit 31 set when the tile is partial.
 Work order (Section IV-C balances the masked work over the pipelines that
 share a broadcast; on a GPU the same concern is load balance across compute
 units): the rows sorted by live count, heaviest first, ties by row number.
+The paper fixes no resolution for "heaviest"; counts are compared through a
+monotone bin code that is exact below 128 and keeps 16 steps per octave
+above (relative resolution 1/16), so that every order uses at most 512 bins.
 """
 from __future__ import annotations
 
@@ -59,10 +62,27 @@ def tile_classes(block_mask, B, Hq, S_q, S_k, blk, causal):
     return live, partial
 
 
+N_BINS = 512
+
+
+def count_bin(counts) -> np.ndarray:
+    """Bin of a live count: the count itself below 128; above, with
+    e = floor(log2 c), 128 + 16*(e - 7) + (the four bits of c below its
+    leading one).  Monotone in c; bins < 512 for every c < 2**31."""
+    c = np.asarray(counts, dtype=np.int64)
+    if np.any(c < 0) or np.any(c >= 2 ** 31):
+        raise ValueError("live counts lie in [0, 2**31)")
+    e = np.zeros_like(c)
+    for k in range(1, 31):                      # e = position of the leading one
+        e += (c >> k) > 0
+    shift = np.maximum(e - 4, 0)
+    big = 128 + 16 * (e - 7) + ((c >> shift) & 15)
+    return np.where(c < 128, c, big)
+
+
 def work_order(counts: np.ndarray) -> np.ndarray:
-    """Rows by live count, heaviest first; equal counts keep row order."""
-    counts = np.asarray(counts, dtype=np.int64)
-    return np.argsort(-counts, kind="stable").astype(np.int32)
+    """Rows by live count bin, heaviest first; equal bins keep row order."""
+    return np.argsort(-count_bin(counts), kind="stable").astype(np.int32)
 
 
 def build_index(block_mask, B, Hq, S_q, S_k, blk=64, causal=True):

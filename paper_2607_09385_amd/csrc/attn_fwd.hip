@@ -34,6 +34,9 @@
 #ifndef STEEL_NT
 #define STEEL_NT 1
 #endif
+#ifndef STEEL_STAGES_SINGLE
+#define STEEL_STAGES_SINGLE 2
+#endif
 #ifndef STEEL_STAGES
 #define STEEL_STAGES 4
 #endif
@@ -135,9 +138,11 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <int P> struct Par { static constexpr int value = P; };
 
-// Depth of the K/V ring (stages of one K tile and one V tile each).
+// Depth of the K/V ring (stages of one K tile and one V tile each).  A
+// single-head workgroup has only two waves, so it keeps the ring short and
+// leaves LDS for more workgroups per CU.
 template <int D, int PACK, int NT>
-constexpr int stages_for() { return STEEL_STAGES; }
+constexpr int stages_for() { return PACK == 1 ? STEEL_STAGES_SINGLE : STEEL_STAGES; }
 
 // Rows per wave: 32 (NT = 1), so that two waves share each SIMD and one can
 // issue MFMAs while the other computes exponentials.

@@ -7,14 +7,18 @@
 // query block: row_ptr (exclusive prefix sum of live counts) and col (live kb,
 // bit 31 = partial).  Section IV-C balances the masked work across the
 // pipelines; the GPU analogue is a work order that hands out the heaviest
-// query blocks first (stable counting sort by live count).
+// query blocks first: a stable counting sort by count_bin of the live count.
 //
-// Kernels, in launch order:
-//   classify : one wave per row: live count; head-pack uniformity flag
-//   hist     : per chunk of 256 items: histogram of count bins (LDS atomics)
-//   scan     : one workgroup: row_ptr, and the chunk bases of each work list
-//   fill     : one wave per row: the live kb list with partial flags
-//   scatter  : per chunk: stable placement of each item in its work order
+// Three launches in the common case (R <= kFastRows rows):
+//   classify     one wave per row, 4 mask bytes per lane: live count, plus
+//                kUniformBit on the first row of a head pack whose members
+//                all have the same live set
+//   scan_small   one workgroup, in LDS: row_ptr, and per work list the
+//                per-chunk bin histograms turned into scatter bases
+//   fill_scatter one wave per row writes its live list; one workgroup per
+//                chunk of 256 items places them in the work order
+// Larger problems build the histograms with one workgroup per chunk and scan
+// them in a separate single-workgroup kernel.
 #include "internal.h"
 
 namespace steel {
@@ -29,182 +33,351 @@ __device__ __forceinline__ bool partial_tile(const Problem& p, int qb, int kb) {
          (long long)(kb + 1) * kBlk > p.S_k;
 }
 
-__device__ __forceinline__ bool tile_live(const Problem& p, const uint8_t* mrow, int qb, int kb) {
-  return kb < p.nKB && (mrow == nullptr || mrow[kb] != 0) && !causal_dead(p, qb, kb);
+// Live bits of tiles (qb, kb0 .. kb0+3) of one row (bit e = tile kb0 + e).
+// wide: the row holds whole 4-byte words (nKB % 4 == 0, aligned mask).
+__device__ __forceinline__ uint32_t live_quad(const Problem& p, const uint8_t* mrow, bool wide,
+                                              int qb, int kb0) {
+  uint32_t bytes;
+  if (mrow == nullptr) {
+    bytes = 0x01010101u;
+  } else if (wide) {
+    bytes = kb0 < p.nKB ? *(const uint32_t*)(mrow + kb0) : 0u;
+  } else {
+    bytes = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (kb0 + e < p.nKB) bytes |= (uint32_t)(mrow[kb0 + e] != 0) << (8 * e);
+  }
+  uint32_t bits = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int kb = kb0 + e;
+    const bool live = kb < p.nKB && ((bytes >> (8 * e)) & 0xffu) != 0 && !causal_dead(p, qb, kb);
+    bits |= (uint32_t)live << e;
+  }
+  return bits;
 }
 
 __global__ __launch_bounds__(256) void k_classify(Problem p, const uint8_t* __restrict__ mask,
-                                                  int32_t* __restrict__ cnt,
-                                                  uint8_t* __restrict__ uni) {
+                                                  int wide, int32_t* __restrict__ cnt) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + wave;
   if (r >= p.R) return;
   const int qb = r % p.nQB;
   const int h = (r / p.nQB) % p.Hq;
   const uint8_t* mrow = mask ? mask + (size_t)r * p.nKB : nullptr;
+  const bool leader = p.pack > 1 && h % p.pack == 0;
   int c = 0;
-  for (int kb0 = 0; kb0 < p.nKB; kb0 += 64)
-    c += __popcll(__ballot(tile_live(p, mrow, qb, kb0 + lane)));
-  if (lane == 0) cnt[r] = c;
-  if (p.pack > 1 && h % p.pack == 0) {
-    bool same = true;
-    if (mrow) {
-      for (int j = 1; j < p.pack && same; ++j) {
-        const uint8_t* mj = mrow + (size_t)j * p.nQB * p.nKB;
-        for (int kb0 = 0; kb0 < p.nKB; kb0 += 64) {
-          const int kb = kb0 + lane;
-          const bool diff = tile_live(p, mrow, qb, kb) != tile_live(p, mj, qb, kb);
-          if (__ballot(diff)) { same = false; break; }
-        }
-      }
-    }
-    if (lane == 0) uni[(size_t)((r / p.nQB) / p.pack) * p.nQB + qb] = same ? 1 : 0;
+  bool same = true;
+  for (int kb0 = 4 * lane; kb0 < p.nKB; kb0 += 256) {
+    const uint32_t bits = live_quad(p, mrow, wide, qb, kb0);
+    c += __popc(bits);
+    if (leader && mrow)
+      for (int j = 1; j < p.pack; ++j)
+        same &= live_quad(p, mrow + (size_t)j * p.nQB * p.nKB, wide, qb, kb0) == bits;
   }
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+  const bool uniform = leader && __ballot(!same) == 0ull;
+  if (lane == 0) cnt[r] = c | (uniform ? (int)kUniformBit : 0);
 }
 
-// Item of a work list: list 0 holds single query-head rows that are not part
-// of a uniform head pack, list 1 holds uniform head packs.
-__device__ __forceinline__ bool item_info(const Problem& p, const int32_t* cnt, const uint8_t* uni,
-                                          int list, int item, int* bin) {
-  int row;
+// Item of a work list: list 0 holds the rows that are not in a uniform head
+// pack, list 1 the uniform packs (item = pack index, its row = its first
+// head's).  Returns false when the item is not in the list.
+__device__ __forceinline__ bool item_info(const Problem& p, const int32_t* cnt, int list, int item,
+                                          int* bin) {
+  int c;
   if (list == 0) {
     if (item >= p.R) return false;
+    c = cnt[item];
     if (p.pack > 1) {
-      const int qb = item % p.nQB;
-      const int pid = ((item / p.nQB) / p.pack) * p.nQB + qb;
-      if (uni[pid]) return false;
+      const int bh = item / p.nQB, qb = item - bh * p.nQB;
+      if (cnt[(bh & ~(p.pack - 1)) * p.nQB + qb] & (int)kUniformBit) return false;
     }
-    row = item;
   } else {
     if (item >= p.NP) return false;
-    if (!uni[item]) return false;
-    const int qb = item % p.nQB;
-    row = (item / p.nQB) * p.pack * p.nQB + qb;
+    const int bh = item / p.nQB, qb = item - bh * p.nQB;
+    c = cnt[bh * p.pack * p.nQB + qb];
+    if (!(c & (int)kUniformBit)) return false;
   }
-  *bin = cnt[row] >> p.bin_shift;
+  *bin = count_bin(c & ~(int)kUniformBit);
   return true;
 }
 
-__global__ __launch_bounds__(256) void k_hist(Problem p, const int32_t* __restrict__ cnt,
-                                              const uint8_t* __restrict__ uni,
-                                              int32_t* __restrict__ hist, int list, int nch) {
-  __shared__ int32_t h[kMaxBins];
-  for (int i = threadIdx.x; i < p.nbins; i += 256) h[i] = 0;
+// Exclusive scan of one value per thread over a 1024-thread workgroup; the
+// sum of all values goes to total.  sh needs 32 ints.
+__device__ int wg_exclusive_scan(int x, int* sh, int& total) {
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  int incl = x;
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(incl, off);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) sh[wave] = incl;
   __syncthreads();
-  int bin;
-  if (item_info(p, cnt, uni, list, blockIdx.x * kChunk + threadIdx.x, &bin)) atomicAdd(&h[bin], 1);
+  if (wave == 0) {
+    int w = lane < 16 ? sh[lane] : 0;
+    for (int off = 1; off < 16; off <<= 1) {
+      const int y = __shfl_up(w, off);
+      if (lane >= off) w += y;
+    }
+    if (lane < 16) sh[16 + lane] = w;  // inclusive wave totals
+  }
   __syncthreads();
-  // bin-major with bins descending, so one linear scan yields heaviest-first bases
-  for (int i = threadIdx.x; i < p.nbins; i += 256)
-    hist[(size_t)(p.nbins - 1 - i) * nch + blockIdx.x] = h[i];
+  const int base = wave > 0 ? sh[16 + wave - 1] : 0;
+  total = sh[31];
+  __syncthreads();  // sh is free again
+  return base + incl - x;
 }
 
-// Exclusive scan of n ints in place (or src -> dst) by one 1024-thread
-// workgroup; returns the total to every thread.
-__device__ int block_exclusive_scan(const int32_t* src, int32_t* dst, long long n, int32_t* sh) {
-  const int t = threadIdx.x;
+// In-place exclusive scan of a[0 .. n) (LDS or global) by a 1024-thread
+// workgroup, contiguous segments per thread; returns the total.
+__device__ int wg_scan_array(int* a, long long n, int* sh) {
   const long long per = (n + 1023) / 1024;
-  const long long lo = min((long long)t * per, n), hi = min(lo + per, n);
+  const long long lo = min((long long)threadIdx.x * per, n), hi = min(lo + per, n);
   int s = 0;
-  for (long long i = lo; i < hi; ++i) s += src[i];
-  sh[t] = s;
-  __syncthreads();
-  for (int off = 1; off < 1024; off <<= 1) {
-    const int v = t >= off ? sh[t - off] : 0;
-    __syncthreads();
-    sh[t] += v;
-    __syncthreads();
-  }
-  int run = sh[t] - s;  // exclusive prefix of this segment
-  const int total = sh[1023];
-  __syncthreads();
+  for (long long i = lo; i < hi; ++i) s += a[i];
+  int total;
+  int run = wg_exclusive_scan(s, sh, total);
   for (long long i = lo; i < hi; ++i) {
-    const int x = src[i];
-    dst[i] = run;
+    const int x = a[i];
+    a[i] = run;
     run += x;
   }
+  __syncthreads();
   return total;
 }
 
-__global__ __launch_bounds__(1024) void k_scan(Problem p, const int32_t* __restrict__ cnt,
-                                               int32_t* __restrict__ row_ptr,
-                                               int32_t* hist_s, long long nh_s,
-                                               int32_t* hist_p, long long nh_p,
-                                               int32_t* __restrict__ n_items) {
-  __shared__ int32_t sh[1024];
-  const int tot = block_exclusive_scan(cnt, row_ptr, p.R, sh);
-  if (threadIdx.x == 0) row_ptr[p.R] = tot;
+__device__ __forceinline__ void write_header(const Problem& p, int32_t* n_items) {
+  n_items[2] = kPlanMagic;
+  n_items[3] = p.R;
+  n_items[4] = p.nKB;
+  n_items[5] = p.pack;
+  n_items[6] = p.causal;
+  n_items[7] = p.delta;
+}
+
+// Histogram index of (bin, chunk): bins descending from the list's top bin,
+// then chunks, so one exclusive scan yields heaviest-first, stable scatter
+// bases.  n_items[kTopBin + list] holds the top bin of each list.
+__device__ __forceinline__ int hist_at(int bin, int chunk, int nch, int top) {
+  return (top - bin) * nch + chunk;
+}
+
+// Common case: one workgroup does the row_ptr scan and the work-order
+// histograms and bases in LDS.
+__global__ __launch_bounds__(1024) void k_scan_small(Problem p, const int32_t* __restrict__ cnt_g,
+                                                     int32_t* __restrict__ row_ptr,
+                                                     int32_t* __restrict__ hist_s,
+                                                     int32_t* __restrict__ hist_p,
+                                                     int32_t* __restrict__ n_items) {
+  __shared__ int cnt[kFastRows];
+  __shared__ int hist[kBins * (kFastRows / kChunk)];
+  __shared__ int sh[32];
+  constexpr int kPerThread = kFastRows / 1024;
+  const int t = threadIdx.x;
+  const int R = p.R;
+  {
+    int v[kPerThread];
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j) {
+      const int i = t + 1024 * j;
+      v[j] = i < R ? cnt_g[i] : 0;
+    }
+#pragma unroll
+    for (int j = 0; j < kPerThread; ++j)
+      if (t + 1024 * j < R) cnt[t + 1024 * j] = v[j];
+  }
   __syncthreads();
-  const int ns = block_exclusive_scan(hist_s, hist_s, nh_s, sh);
+
+  // row_ptr: prefix sums in hist (free so far), then stored coalesced
+  for (int i = t; i < R; i += 1024) hist[i] = cnt[i] & ~(int)kUniformBit;
   __syncthreads();
-  const int np = nh_p > 0 ? block_exclusive_scan(hist_p, hist_p, nh_p, sh) : 0;
+  const int total = wg_scan_array(hist, R, sh);
+  for (int i = t; i < R; i += 1024) row_ptr[i] = hist[i];
+  if (t == 0) row_ptr[R] = total;
+  __syncthreads();
+
+  const int pmask = ~(p.pack - 1);  // pack is 1, 2 or 4
+  const int dq = 1024 / p.nQB, dr = 1024 % p.nQB;
+  for (int list = 0; list < 2; ++list) {
+    const int n_all = list == 0 ? R : (p.pack > 1 ? p.NP : 0);
+    const int nch = nchunks(n_all);
+    // items t, t+1024, ...: (bh, qb) stepped by (dq, dr) instead of divided;
+    // first the top bin of the list, then the histogram below it
+    auto walk = [&](auto&& fn) {
+      int bh = t / p.nQB, qb = t - bh * p.nQB;
+      for (int i = t; i < n_all; i += 1024) {
+        int c;
+        bool present;
+        if (list == 0) {
+          c = cnt[i];
+          present = p.pack == 1 || !(cnt[(bh & pmask) * p.nQB + qb] & (int)kUniformBit);
+        } else {
+          c = cnt[bh * p.pack * p.nQB + qb];
+          present = (c & (int)kUniformBit) != 0;
+        }
+        if (present) fn(i, count_bin(c & ~(int)kUniformBit));
+        qb += dr;
+        bh += dq;
+        if (qb >= p.nQB) {
+          qb -= p.nQB;
+          ++bh;
+        }
+      }
+    };
+    int top = -1;
+    walk([&](int, int bin) { top = max(top, bin); });
+    for (int off = 32; off > 0; off >>= 1) top = max(top, __shfl_xor(top, off));
+    if ((t & 63) == 0) sh[t >> 6] = top;
+    __syncthreads();
+    top = -1;
+    for (int w = 0; w < 16; ++w) top = max(top, sh[w]);
+    __syncthreads();
+    if (top < 0) {  // no item in this list
+      if (t == 0) {
+        n_items[list] = 0;
+        n_items[kTopBin + list] = -1;
+      }
+      continue;
+    }
+    const int E = (top + 1) * nch;
+    for (int i = t; i < E; i += 1024) hist[i] = 0;
+    __syncthreads();
+    walk([&](int i, int bin) { atomicAdd(&hist[hist_at(bin, i / kChunk, nch, top)], 1); });
+    __syncthreads();
+    const int n = wg_scan_array(hist, E, sh);
+    int32_t* g = list == 0 ? hist_s : hist_p;
+    for (int i = t; i < E; i += 1024) g[i] = hist[i];
+    if (t == 0) {
+      n_items[list] = n;
+      n_items[kTopBin + list] = top;
+    }
+    __syncthreads();
+  }
+  if (t == 0) write_header(p, n_items);
+}
+
+// Larger problems: per-chunk histograms ...
+__global__ __launch_bounds__(256) void k_hist(Problem p, const int32_t* __restrict__ cnt,
+                                              int32_t* __restrict__ hist, int list, int nch) {
+  __shared__ int h[kBins];
+  for (int i = threadIdx.x; i < kBins; i += 256) h[i] = 0;
+  __syncthreads();
+  int bin;
+  if (item_info(p, cnt, list, blockIdx.x * kChunk + threadIdx.x, &bin)) atomicAdd(&h[bin], 1);
+  __syncthreads();
+  for (int i = threadIdx.x; i < kBins; i += 256) hist[hist_at(i, blockIdx.x, nch, kBins - 1)] = h[i];
+}
+
+// ... and one workgroup scanning them and the counts in global memory.
+__global__ __launch_bounds__(1024) void k_scan_large(Problem p, const int32_t* __restrict__ cnt,
+                                                     int32_t* __restrict__ row_ptr,
+                                                     int32_t* hist_s, long long nh_s,
+                                                     int32_t* hist_p, long long nh_p,
+                                                     int32_t* __restrict__ n_items) {
+  __shared__ int sh[32];
+  for (long long i = threadIdx.x; i < p.R; i += 1024) row_ptr[i] = cnt[i] & ~(int)kUniformBit;
+  __syncthreads();
+  const int tot = wg_scan_array(row_ptr, p.R, sh);
+  const int ns = wg_scan_array(hist_s, nh_s, sh);
+  const int np = nh_p > 0 ? wg_scan_array(hist_p, nh_p, sh) : 0;
   if (threadIdx.x == 0) {
+    row_ptr[p.R] = tot;
     n_items[0] = ns;
     n_items[1] = np;
-    n_items[2] = kPlanMagic;
-    n_items[3] = p.R;
-    n_items[4] = p.nKB;
-    n_items[5] = p.pack;
-    n_items[6] = p.causal;
-    n_items[7] = p.delta;
+    n_items[kTopBin] = kBins - 1;
+    n_items[kTopBin + 1] = kBins - 1;
+    write_header(p, n_items);
   }
 }
 
-__global__ __launch_bounds__(256) void k_fill(Problem p, const uint8_t* __restrict__ mask,
-                                              const int32_t* __restrict__ row_ptr,
-                                              uint32_t* __restrict__ col) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + wave;
-  if (r >= p.R) return;
-  const int qb = r % p.nQB;
-  const uint8_t* mrow = mask ? mask + (size_t)r * p.nKB : nullptr;
-  int pos = row_ptr[r];
-  const unsigned long long below = (1ull << lane) - 1ull;
-  for (int kb0 = 0; kb0 < p.nKB; kb0 += 64) {
-    const int kb = kb0 + lane;
-    const bool live = tile_live(p, mrow, qb, kb);
-    const unsigned long long bal = __ballot(live);
-    if (live)
-      col[pos + __popcll(bal & below)] =
-          (uint32_t)kb | (partial_tile(p, qb, kb) ? 0x80000000u : 0u);
-    pos += __popcll(bal);
-  }
-}
-
-__global__ __launch_bounds__(256) void k_scatter(Problem p, const int32_t* __restrict__ cnt,
-                                                 const uint8_t* __restrict__ uni,
-                                                 const int32_t* __restrict__ base, int list,
-                                                 int nch, int32_t* __restrict__ order) {
-  __shared__ int32_t bins[kChunk];
+// Workgroups [0, rows_grid): one wave per row writes the live list of the
+// row at row_ptr[r].  The rest: one workgroup per chunk of 256 items of a
+// work list puts each present item at its bin's base for the chunk plus its
+// rank among the chunk's earlier items of the same bin.
+__global__ __launch_bounds__(256) void k_fill_scatter(
+    Problem p, const uint8_t* __restrict__ mask, int wide, const int32_t* __restrict__ cnt,
+    const int32_t* __restrict__ row_ptr, uint32_t* __restrict__ col,
+    const int32_t* __restrict__ hist_s, const int32_t* __restrict__ hist_p,
+    const int32_t* __restrict__ n_items, int32_t* __restrict__ order_s,
+    int32_t* __restrict__ order_p, int rows_grid, int nch_s) {
+  __shared__ int bins[kChunk];
   const int t = threadIdx.x;
-  const int item = blockIdx.x * kChunk + t;
+  if ((int)blockIdx.x < rows_grid) {
+    const int wave = t >> 6, lane = t & 63;
+    const int r = blockIdx.x * 4 + wave;
+    if (r >= p.R) return;
+    const int qb = r % p.nQB;
+    const uint8_t* mrow = mask ? mask + (size_t)r * p.nKB : nullptr;
+    int pos = row_ptr[r];
+    for (int kb0 = 4 * lane; kb0 - 4 * lane < p.nKB; kb0 += 256) {
+      const uint32_t bits = kb0 < p.nKB ? live_quad(p, mrow, wide, qb, kb0) : 0u;
+      // this 256-block's entries in kb order: lane-major, 4 per lane
+      const int mine = __popc(bits);
+      int before = mine;
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(before, off);
+        if (lane >= off) before += y;
+      }
+      const int total = __shfl(before, 63);
+      int k = pos + before - mine;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        if ((bits >> e) & 1u) {
+          const int kb = kb0 + e;
+          col[k++] = (uint32_t)kb | (partial_tile(p, qb, kb) ? 0x80000000u : 0u);
+        }
+      pos += total;
+    }
+    return;
+  }
+  int c = (int)blockIdx.x - rows_grid;
+  int list = 0, nch = nch_s;
+  if (c >= nch_s) {
+    list = 1;
+    c -= nch_s;
+    nch = nchunks(p.NP);
+  }
+  const int top = n_items[kTopBin + list];
+  const int item = c * kChunk + t;
   int bin = -1;
-  const bool present = item_info(p, cnt, uni, list, item, &bin);
+  const bool present = top >= 0 && item_info(p, cnt, list, item, &bin);
   bins[t] = present ? bin : -1;
   __syncthreads();
   if (!present) return;
   int rank = 0;
-  for (int j = 0; j < t; ++j) rank += bins[j] == bin;
-  order[base[(size_t)(p.nbins - 1 - bin) * nch + blockIdx.x] + rank] = item;
+  const int4* b4 = reinterpret_cast<const int4*>(bins);
+  for (int j = 0; j < (t >> 2); ++j) {
+    const int4 v = b4[j];
+    rank += (v.x == bin) + (v.y == bin) + (v.z == bin) + (v.w == bin);
+  }
+  for (int j = t & ~3; j < t; ++j) rank += bins[j] == bin;
+  const int32_t* base = list == 0 ? hist_s : hist_p;
+  int32_t* order = list == 0 ? order_s : order_p;
+  order[base[hist_at(bin, c, nch, top)] + rank] = item;
 }
 
 hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const IndexBuffers& w,
                               hipStream_t s) {
+  const int wide = mask == nullptr || ((p.nKB % 4) == 0 && ((uintptr_t)mask & 3u) == 0);
+  const int rows_grid = (p.R + 3) / 4;
   const int nch_s = nchunks(p.R);
   const int nch_p = p.pack > 1 ? nchunks(p.NP) : 0;
-  const int rows_grid = (p.R + 3) / 4;
-  hipLaunchKernelGGL(k_classify, dim3(rows_grid), dim3(256), 0, s, p, mask, w.cnt, w.uni);
-  hipLaunchKernelGGL(k_hist, dim3(nch_s), dim3(256), 0, s, p, w.cnt, w.uni, w.hist_s, 0, nch_s);
-  if (nch_p)
-    hipLaunchKernelGGL(k_hist, dim3(nch_p), dim3(256), 0, s, p, w.cnt, w.uni, w.hist_p, 1, nch_p);
-  hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, s, p, w.cnt, w.row_ptr, w.hist_s,
-                     (long long)p.nbins * nch_s, w.hist_p, (long long)p.nbins * nch_p, w.n_items);
-  hipLaunchKernelGGL(k_fill, dim3(rows_grid), dim3(256), 0, s, p, mask, w.row_ptr, w.col);
-  hipLaunchKernelGGL(k_scatter, dim3(nch_s), dim3(256), 0, s, p, w.cnt, w.uni, w.hist_s, 0, nch_s,
-                     w.order_s);
-  if (nch_p)
-    hipLaunchKernelGGL(k_scatter, dim3(nch_p), dim3(256), 0, s, p, w.cnt, w.uni, w.hist_p, 1,
-                       nch_p, w.order_p);
+  hipLaunchKernelGGL(k_classify, dim3(rows_grid), dim3(256), 0, s, p, mask, wide, w.cnt);
+  if (p.R <= kFastRows) {
+    hipLaunchKernelGGL(k_scan_small, dim3(1), dim3(1024), 0, s, p, w.cnt, w.row_ptr, w.hist_s,
+                       w.hist_p, w.n_items);
+  } else {
+    hipLaunchKernelGGL(k_hist, dim3(nch_s), dim3(256), 0, s, p, w.cnt, w.hist_s, 0, nch_s);
+    if (nch_p)
+      hipLaunchKernelGGL(k_hist, dim3(nch_p), dim3(256), 0, s, p, w.cnt, w.hist_p, 1, nch_p);
+    hipLaunchKernelGGL(k_scan_large, dim3(1), dim3(1024), 0, s, p, w.cnt, w.row_ptr, w.hist_s,
+                       (long long)kBins * nch_s, w.hist_p, (long long)kBins * nch_p, w.n_items);
+  }
+  hipLaunchKernelGGL(k_fill_scatter, dim3(rows_grid + nch_s + nch_p), dim3(256), 0, s, p, mask,
+                     wide, w.cnt, w.row_ptr, w.col, w.hist_s, w.hist_p, w.n_items, w.order_s,
+                     w.order_p, rows_grid, nch_s);
   return hipGetLastError();
 }
 

@@ -7,8 +7,18 @@
 namespace steel {
 
 constexpr int kBlk = 64;          // mask block edge = tile edge
-constexpr int kMaxBins = 4096;    // work-order histogram bins
+constexpr int kBins = 512;        // work-order bins (count_bin < kBins)
 constexpr int kChunk = 256;       // items per work-order chunk
+
+// Work-order bin of a live count c in [0, 2^31): c itself below 128; above,
+// 16 bins per octave, 128 + 16*(e - 7) + (the 4 bits below the leading one),
+// e = floor(log2 c).  Monotone in c, exact where the counts are small, and
+// within 1/16 of the count where they are large.
+__host__ __device__ inline int count_bin(int c) {
+  if (c < 128) return c;
+  const int e = 31 - __builtin_clz((unsigned)c);
+  return 128 + 16 * (e - 7) + ((c >> (e - 4)) & 15);
+}
 
 // Problem description shared by the index build and the attention kernels.
 struct Problem {
@@ -20,29 +30,36 @@ struct Problem {
   int delta;    // S_k - S_q
   int R;        // B*Hq*nQB rows of the live-block list
   int NP;       // B*(Hq/pack)*nQB head packs (0 when pack == 1)
-  int bin_shift;
-  int nbins;
 };
 
 // Device workspace of one call.
 struct IndexBuffers {
-  int32_t* cnt;        // [R]   live blocks per row
-  uint8_t* uni;        // [NP]  1 if the pack's rows have identical live lists
-  int32_t* hist_s;     // [nbins * nchunk_s]  per-chunk bin counts, then bases
-  int32_t* hist_p;     // [nbins * nchunk_p]
+  int32_t* cnt;        // [R]   live blocks per row (| kUniformBit, see below)
+  int32_t* hist_s;     // [kBins * nchunk_s]  per-chunk bin counts, then bases
+  int32_t* hist_p;     // [kBins * nchunk_p]
   int32_t* row_ptr;    // [R+1]
   uint32_t* col;       // [R*nKB] capacity
   int32_t* order_s;    // [R]   single-head items, heaviest first
   int32_t* order_p;    // [NP]  head-pack items, heaviest first
-  int32_t* n_items;    // [8]   {single items, pack items, plan header ...}
+  int32_t* n_items;    // [kHeaderInts] {single items, pack items, plan header,
+                       //   top bins of the two lists}
 };
 
 // Plan header written after the two item counts; the attention kernels check
 // it against their own arguments before touching the index.
 constexpr int kPlanMagic = 0x5354454c;  // "STEL"
-constexpr int kHeaderInts = 8;
+constexpr int kTopBin = 8;
+constexpr int kHeaderInts = 10;
 
-inline int nchunks(int n) { return (n + kChunk - 1) / kChunk; }
+__host__ __device__ inline int nchunks(int n) { return (n + kChunk - 1) / kChunk; }
+
+// Set in cnt[r] of the first row of a head pack whose rows all have the same
+// live list (counts are below 2^30: R * nKB < 2^31).
+constexpr uint32_t kUniformBit = 1u << 30;
+
+// Up to this many rows one workgroup scans the counts and the work-order
+// histograms in LDS (4 + 4 * kBins / kChunk = 12 bytes per row: 144 KiB).
+constexpr int kFastRows = 12288;
 
 // Enqueue the index build.  With p.pack == 1 every row is a single-head item.
 hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const IndexBuffers& w,

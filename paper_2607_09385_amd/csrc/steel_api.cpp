@@ -94,10 +94,6 @@ int check_shape(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
   p->causal = causal;
   p->delta = S_k - S_q;
   p->R = (int)R;
-  int shift = 0;
-  while (((p->nKB >> shift) + 1) > steel::kMaxBins) ++shift;
-  p->bin_shift = shift;
-  p->nbins = (p->nKB >> shift) + 1;
   p->pack = 1;
   p->NP = 0;
   return STEEL_OK;
@@ -106,7 +102,7 @@ int check_shape(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cnt, uni, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, total;
+  size_t cnt, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, total;
 };
 
 Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
@@ -120,9 +116,8 @@ Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
   const size_t nch_s = steel::nchunks(p.R);
   const size_t nch_p = p.pack > 1 ? steel::nchunks(p.NP) : 0;
   L.cnt = take(sizeof(int32_t) * p.R);
-  L.uni = take(p.NP > 0 ? (size_t)p.NP : 1);
-  L.hist_s = take(sizeof(int32_t) * p.nbins * nch_s);
-  L.hist_p = take(sizeof(int32_t) * (nch_p ? p.nbins * nch_p : 1));
+  L.hist_s = take(sizeof(int32_t) * steel::kBins * nch_s);
+  L.hist_p = take(sizeof(int32_t) * (nch_p ? steel::kBins * nch_p : 1));
   L.n_items = take(sizeof(int32_t) * steel::kHeaderInts);
   L.order_p = take(sizeof(int32_t) * (p.NP > 0 ? p.NP : 1));
   if (with_rowptr_col_order) {
@@ -168,7 +163,6 @@ void set_pack(steel::Problem* p) {
 steel::IndexBuffers carve(char* ws, const Layout& L) {
   steel::IndexBuffers w;
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
-  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
   w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
   w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);
@@ -289,7 +283,6 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   if (e != hipSuccess) return hip_fail(e, "allocating workspace");
   steel::IndexBuffers w;
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
-  w.uni = reinterpret_cast<uint8_t*>(ws + L.uni);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
   w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
   w.n_items = reinterpret_cast<int32_t*>(ws + L.n_items);

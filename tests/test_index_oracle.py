@@ -79,8 +79,44 @@ def test_csr_structure(case):
         assert kbs == [kb for kb in range(nKB) if live2[r, kb]]
         assert [(int(c) >> 31) == 1 for c in seg] == [bool(part2[r, kb]) for kb in kbs]
     counts = np.diff(row_ptr)
+    assert counts.max() < 128          # the bin code is the identity here
     want = sorted(range(len(counts)), key=lambda r: (-counts[r], r))
     assert order.tolist() == want
+
+
+def brute_bin(c):
+    """The bin code from its definition, on Python ints."""
+    if c < 128:
+        return c
+    e = c.bit_length() - 1
+    return 128 + 16 * (e - 7) + ((c >> (e - 4)) & 15)
+
+
+def test_count_bin_closed_forms():
+    cs = list(range(0, 5000)) + [2 ** k + d for k in range(12, 31) for d in (-1, 0, 1)] + [2 ** 31 - 1]
+    got = oracle.count_bin(np.array(cs)).tolist()
+    assert got == [brute_bin(c) for c in cs]
+    assert got[:128] == list(range(128))
+    # octave starts: 128 -> 128, 256 -> 144, 512 -> 160; last bin of 2**31 - 1
+    assert [brute_bin(c) for c in (128, 255, 256, 511, 512)] == [128, 143, 144, 159, 160]
+    assert brute_bin(2 ** 31 - 1) == oracle.N_BINS - 1
+    # monotone, and one bin never spans more than 1/16 of its smallest count
+    assert all(a <= b for a, b in zip(got[:5000], got[1:5000]))
+    lo = {}
+    for c in range(128, 5000):
+        lo.setdefault(brute_bin(c), c)
+    for c in range(128, 5000):
+        assert c - lo[brute_bin(c)] < lo[brute_bin(c)] / 16
+    with pytest.raises(ValueError):
+        oracle.count_bin([2 ** 31])
+
+
+def test_work_order_bins_large_counts():
+    # 130, 135 and 129 share bin 128; 200 is bin 137; 127 is bin 127
+    counts = np.array([130, 200, 135, 127, 129, 300])
+    assert oracle.work_order(counts).tolist() == [5, 1, 0, 2, 4, 3]
+    # the plain count sort would put 135 before 130: the bins keep row order
+    assert np.argsort(-counts, kind="stable").tolist() == [5, 1, 2, 0, 4, 3]
 
 
 def test_live_count_closed_forms():
