@@ -125,6 +125,82 @@ def cpu_baseline(cfg, q, k, v, mask, counts, seconds):
     }
 
 
+COPY_BYTES = 256 << 20   # reference elementwise kernel for the counter scale
+
+
+def traffic_run(name, runs):
+    """Workload for the rocprofv3 counter passes: the attention run of one
+    plan ``runs`` times, then one float32 elementwise kernel that reads and
+    writes exactly COPY_BYTES each (its counter readings give the scale from
+    counter KiB to bytes)."""
+    import torch
+    import workloads
+    import paper_2607_09385_amd as steel
+
+    steel.load()
+    cfg = workloads.CONFIGS[name]
+    q, k, v, mask = workloads.make_workload(cfg)
+    dev = torch.device("cuda:0")
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    md = None if mask is None else torch.from_numpy(mask).to(dev)
+    out = torch.empty((cfg.B, cfg.Hq, cfg.S_q, cfg.D), dtype=torch.float32, device=dev)
+    plan = steel.Plan(md, cfg.B, cfg.Hq, cfg.Hkv, cfg.S_q, cfg.S_k, causal=cfg.causal, device=dev)
+    for _ in range(runs):
+        plan.run(qd, kd, vd, scale=cfg.scale, out=out)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    torch.add(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(f"[traffic-run] {name}: {runs} attention runs, then one {COPY_BYTES} B elementwise add",
+          flush=True)
+
+
+def traffic_from(fetch_dir, write_dir, name):
+    """Turn the two counter passes over ``--traffic-run`` into HBM bytes per
+    attention run and record them in profiles/attn_traffic.json."""
+    import csv
+
+    def per_kernel(d, counter):
+        vals = {}
+        for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv"))):
+            if r["Counter_Name"] != counter:
+                continue
+            vals.setdefault(r["Kernel_Name"].split("(")[0], []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in vals.items()}
+
+    rec = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        k = per_kernel(d, counter)
+        ref = [v for n, v in k.items() if "elementwise" in n]
+        attn = {n: v for n, v in k.items() if "k_attn" in n}
+        scale = COPY_BYTES / (ref[0] * 1024.0)
+        rec[counter] = {"scale": scale,
+                        "kernels": {n: v * 1024.0 * scale for n, v in attn.items()}}
+    kernels = sorted(rec["FETCH_SIZE"]["kernels"])
+    per_run = sum(rec["FETCH_SIZE"]["kernels"][n] + rec["WRITE_SIZE"]["kernels"].get(n, 0.0)
+                  for n in kernels)
+    try:
+        with open(TRAFFIC_FILE) as f:
+            out = json.load(f)
+        if out.get("kernel_sha") != kernel_hash():
+            out = {}
+    except (OSError, ValueError):
+        out = {}
+    out["kernel_sha"] = kernel_hash()
+    out.setdefault("workloads", {})[name] = {
+        "bytes_per_run": per_run,
+        "fetch_bytes": rec["FETCH_SIZE"]["kernels"],
+        "write_bytes": rec["WRITE_SIZE"]["kernels"],
+        "scale_fetch": rec["FETCH_SIZE"]["scale"],
+        "scale_write": rec["WRITE_SIZE"]["scale"],
+        "reference": f"float32 elementwise add reading and writing {COPY_BYTES} B",
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    print(json.dumps(out["workloads"][name], indent=1))
+
+
 def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
     import torch
     import workloads
@@ -219,13 +295,23 @@ def main():
     ap.add_argument("--all", action="store_true", help="one line per named workload")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="workload for the rocprofv3 FETCH_SIZE / WRITE_SIZE passes")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="record HBM bytes per run from the two counter passes")
     args = ap.parse_args()
+    if args.traffic_from:
+        traffic_from(args.traffic_from[0], args.traffic_from[1], args.workload)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, "
               f"WORLD_SIZE={world}); the path shards by head/group with no exchange, "
               "which is described but not run here", file=sys.stderr)
         sys.exit(2)
+    if args.traffic_run:
+        traffic_run(args.workload, args.steps if args.steps != 50 else 5)
+        return
     import workloads
     names = workloads.CONFIG_ORDER if args.all else [args.workload]
     for i, name in enumerate(names):

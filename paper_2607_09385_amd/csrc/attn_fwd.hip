@@ -132,6 +132,26 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
+// Workgroups are dealt to the 8 XCDs round-robin (workgroup b runs on XCD
+// b % 8).  Work-order position of workgroup b: the order is cut into groups
+// of kXcdGroup consecutive items, group g goes to XCD g % 8, and each XCD
+// takes its groups in order.  Neighbouring items of one head pack (adjacent
+// query blocks, mostly the same key/value tiles) then share one XCD's L2,
+// while every XCD still works from the heavy end of the order first.  The
+// grid is a multiple of 8 * kXcdGroup; positions past the item count exit.
+#ifndef STEEL_XCD_GROUP
+#define STEEL_XCD_GROUP 16
+#endif
+constexpr int kXcdGroup = STEEL_XCD_GROUP;
+__device__ __forceinline__ int xcd_slot(int b) {
+  const int x = b & 7, j = b >> 3;
+  return ((j / kXcdGroup) * 8 + x) * kXcdGroup + j % kXcdGroup;
+}
+inline int xcd_grid(int n) {
+  const int m = 8 * kXcdGroup;
+  return (n + m - 1) / m * m;
+}
+
 typedef const __attribute__((address_space(4))) int32_t* cint_p;
 typedef const __attribute__((address_space(4))) uint32_t* cuint_p;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -176,8 +196,9 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
   if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
       hd[4] != a.causal || hd[5] != a.delta)
     return;  // index was planned for another problem: leave out untouched
-  if ((int)blockIdx.x >= ((cint_p)a.n_items)[0]) return;
-  const int item = ((cint_p)a.order)[blockIdx.x];
+  const int idx = xcd_slot((int)blockIdx.x);
+  if (idx >= ((cint_p)a.n_items)[0]) return;
+  const int item = ((cint_p)a.order)[idx];
   const int qb = item % a.nQB;
   const int bh0 = (item / a.nQB) * PACK;  // b*Hq + first head
   const int b = bh0 / a.Hq;
@@ -505,7 +526,8 @@ template <int D, int PACK>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   constexpr int NT = nt_for<D>();
   if (grid > 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, NT>), dim3(grid), dim3(64 * PACK * (2 / NT)), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, NT>), dim3(xcd_grid(grid)), dim3(64 * PACK * (2 / NT)), 0,
+                       s, a);
 }
 
 template <int D>
