@@ -172,7 +172,7 @@ def traffic_from(fetch_dir, write_dir, name):
     rec = {}
     for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         k = per_kernel(d, counter)
-        ref = [v for n, v in k.items() if "elementwise" in n]
+        ref = [v for n, v in k.items() if "elementwise" in n and "add" in n]
         attn = {n: v for n, v in k.items() if "k_attn" in n}
         scale = COPY_BYTES / (ref[0] * 1024.0)
         rec[counter] = {"scale": scale,
