@@ -18,7 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsteel.so")
-SOURCES = ["steel_api.cpp", "block_index.hip", "attn_fwd.hip"]
+SOURCES = ["steel_api.cpp", "block_index.hip", "attn_fwd.hip", "attn_w64.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of every code object: the compiler would
@@ -27,10 +27,13 @@ COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wno-unused-command-line-argument",
-    # keep MFMA accumulators in VGPRs: the softmax reads the scores with VALU
-    # instructions, and AGPR-resident accumulators cost a copy per element
-    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
+# Both attention sources keep the compiler's MFMA accumulators in VGPRs: the
+# softmax reads the scores with VALU instructions, and AGPR-resident scores
+# would cost a copy per element.  (attn_w64.hip places its output
+# accumulator in AGPRs itself.)
+PER_SOURCE = {"attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+              "attn_w64.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:
@@ -43,7 +46,8 @@ def hipcc() -> str:
 def _compile(src: str, extra: list[str]) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [hipcc(), *COMMON, *extra, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *COMMON, *PER_SOURCE.get(src, []), *extra, *lang, "-c", os.path.join(CSRC, src),
+           "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

@@ -1,0 +1,530 @@
+// Fused sparse attention forward for head packs of 4 on gfx950: one wave per
+// query head, 64 rows per wave, software-pipelined, persistent.
+//
+// Same mathematics as k_attn (the online-softmax recurrence of Algorithm 1
+// over the live tiles of a query block, Section IV-A masking, Section IV-C
+// work order), with a different schedule:
+//
+// * Each wave owns all 64 rows of its head (two 32-row MFMA N-tiles), so
+//   every K or V fragment read from LDS feeds two MFMAs: half the LDS read
+//   traffic of 32-row waves.  One wave per SIMD; the MFMA accumulators (S of
+//   two tiles and O) live in AGPRs.
+// * Software pipeline over the tiles i of an item: iteration i runs the
+//   softmax of S_i on the VALU while the matrix core computes S_{i+1} =
+//   K_{i+1} Q^T and O += V_{i-1} P_{i-1}.  The three streams are interleaved
+//   in 32 slots of two MFMAs each, so one wave keeps the matrix core and the
+//   VALU busy at the same time (the paper's three pipeline stages, Algorithm
+//   1, running concurrently inside one wavefront).
+// * K/V tiles flow through a 5-stage LDS ring (160 KiB) in one stream across
+//   the workgroup's items: while an item finishes, the first tiles of the
+//   next one are already being copied, and its Q rows are loaded during the
+//   last iteration.
+// * One workgroup per CU; each takes one item per round of its XCD's share
+//   of the work order (the same XCD-aware placement as k_attn), serpentine
+//   over rounds.
+//
+// Ring: during iteration i the tiles i-1 (V), i (V, next iteration) and i+1
+// (K now, V later) are live; the stage of tile i-2 is refilled with tile i+3,
+// which is first read (K) in iteration i+2.  Every wave waits for its own
+// copies before the barrier that ends an iteration.
+#include <utility>
+
+#include "attn_common.h"
+
+namespace steel {
+
+namespace {
+
+// f(Par<0>{}), f(Par<1>{}), ..., f(Par<N-1>{}): a loop whose index is a
+// compile-time constant in every copy of the body.
+template <typename F, int... S>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, S...>) {
+  (f(Par<S>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+constexpr int kW64Stages = 5;
+
+// s_waitcnt vmcnt(n) for a count known at run time (n <= 2 tiles of copies);
+// larger values wait for everything.
+__device__ __forceinline__ void wait_vm_upto(int n) {
+  switch (n) {
+    case 8: wait_vm<8>(); break;
+    case 16: wait_vm<16>(); break;
+    default: wait_vm<0>(); break;
+  }
+}
+
+// Read one accumulator element where it is used: the scores stay in AGPRs
+// and only the values a softmax step needs pass through VGPRs.
+__device__ __forceinline__ float acc_read(float x) {
+  float r;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(x));
+  return r;
+}
+__device__ __forceinline__ float acc_write(float v) {
+  float r;
+  asm volatile("v_accvgpr_write_b32 %0, %1" : "=a"(r) : "v"(v));
+  return r;
+}
+
+// O += A B on the matrix core with the accumulator in AGPRs.  The scores
+// use the compiler's MFMA (built with VGPR accumulators, read by the
+// softmax), the output accumulator stays in AGPRs: it is only read by the
+// rescale and the epilogue, through acc_read after explicit waits.  In-place
+// accumulation chains are at least 8 MFMAs apart.
+__device__ __forceinline__ void mfma_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+}  // namespace
+
+template <int D>
+__global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
+  constexpr int NW = 4;             // waves = query heads of the pack
+  constexpr int C = D / 8;          // 16-byte chunks per row
+  constexpr int TE = kBlk * D;      // bf16 elements per tile
+  constexpr int TB = TE * 2;        // bytes per tile
+  constexpr int LPW = C / NW;       // copies per lane per tile and tensor
+  constexpr int KS = D / 16;        // k-steps of S^T = K Q^T
+  constexpr int DT = D / 32;        // d tiles of O^T
+  constexpr int ST = kW64Stages;
+  constexpr int CPT = 2 * LPW;      // copy instructions per lane per tile
+  constexpr float TAU = 8.0f;       // rescale only when a row max grows by > 2^8
+  static_assert(D == 128 && CPT == 8, "tuned for D = 128");
+  static_assert(2 * KS * 2 == 32 && 4 * DT * 2 == 32, "32 slots of one QK and one PV MFMA");
+  __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
+
+  const cint_p hd = (cint_p)a.header;
+  if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
+      hd[4] != a.causal || hd[5] != a.delta)
+    return;  // index was planned for another problem: leave out untouched
+  const int n_all = ((cint_p)a.n_items)[0];
+
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int n = lane & 31, hf = lane >> 5;
+  const int xb = (int)blockIdx.x & 7, wb = (int)blockIdx.x >> 3, nwb = (int)gridDim.x >> 3;
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
+
+  // copy plan: copy j of this lane fills tile slot (wave*LPW + j)*64 + lane,
+  // i.e. row (wave*LPW + j)*64/C + lane/C, chunk lane%C (C divides 64)
+  static_assert(64 % C == 0, "whole rows per copy instruction");
+  const int cp_r0 = lane / C, cp_c = lane % C;
+  auto cp_row = [&](int j) __attribute__((always_inline)) { return (wave * LPW + j) * (64 / C) + cp_r0; };
+  auto cp_off = [&](int j) __attribute__((always_inline)) {
+    const int r = cp_row(j);
+    return (uint32_t)((r * D + (cp_c ^ swz<D>(r)) * 8) * 2);
+  };
+  // LDS read offsets (bytes within a tile): K fragment (sg, ks) and the two
+  // transposed halves of V fragment (chunk, dt)
+  uint32_t koff[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = (uint32_t)tile_elem<D>(n, 2 * ks + hf) * 2;
+  const int tg = lane >> 4, tr = (lane >> 2) & 3, tq = lane & 3;
+  uint32_t voff[2][DT];
+#pragma unroll
+  for (int cc = 0; cc < 2; ++cc)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int row = 8 * cc + 4 * (tg >> 1) + tr;
+      voff[cc][dt] = (uint32_t)(tile_elem<D>(row, 4 * dt + 2 * (tg & 1) + (tq >> 1)) + 4 * (tq & 1)) * 2;
+    }
+
+  // ---- work items ----
+  struct Item {
+    int L, beg, qb, b, h0;
+    const __bf16* kg;
+    const __bf16* vg;
+  };
+  // The k-th item of this workgroup is position j of its XCD's share of the
+  // work order, j = k*nwb + w for even k and k*nwb + (nwb-1-w) for odd k
+  // (serpentine): the share is sorted heaviest first, so a workgroup that
+  // takes a heavy item in one round takes a light one in the next.
+  auto decode = [&](int k, Item& it) __attribute__((always_inline)) -> bool {
+    const int j = k * nwb + ((k & 1) ? nwb - 1 - wb : wb);
+    const int idx = xcd_slot(8 * j + xb);
+    if (idx >= n_all) return false;
+    const int item = ((cint_p)a.order)[idx];
+    it.qb = item % a.nQB;
+    const int bh0 = (item / a.nQB) * 4;
+    it.b = bh0 / a.Hq;
+    const int h0 = bh0 % a.Hq;
+    it.h0 = h0;
+    const int r0 = bh0 * a.nQB + it.qb;
+    it.beg = ((cint_p)a.row_ptr)[r0];
+    it.L = ((cint_p)a.row_ptr)[r0 + 1] - it.beg;
+    const size_t kvoff = ((size_t)it.b * a.Hkv + h0 / a.G) * a.S_k * D;
+    it.kg = a.k + kvoff;
+    it.vg = a.v + kvoff;
+    return true;
+  };
+
+  auto issue_copy = [&](const __bf16* src, uint32_t dst, int kb) __attribute__((always_inline)) {
+    const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW) * 1024u;
+    if ((kb + 1) * kBlk <= a.S_k) {
+      const __bf16* sb = src + (size_t)kb * kBlk * D;
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) copy16_to_lds(sb, cp_off(j), lbase + j * 1024u);
+    } else {
+#pragma unroll
+      for (int j = 0; j < LPW; ++j) {
+        const int key = min(kb * kBlk + cp_row(j), a.S_k - 1);
+        const uint32_t off = cp_off(j) + (uint32_t)((key - cp_row(j)) * D * 2);
+        copy16_to_lds(src, off, lbase + j * 1024u);
+      }
+    }
+  };
+  auto issue_tile = [&](const Item& it, int stage, int kb) __attribute__((always_inline)) {
+    issue_copy(it.kg, (uint32_t)(2 * stage) * TB, kb);
+    issue_copy(it.vg, (uint32_t)(2 * stage + 1) * TB, kb);
+  };
+  // live-list entry t of an item (t < 64 for the look-ahead of the next
+  // item; the current item keeps a 128-entry window in two VGPRs)
+  auto load_entry_vec = [&](const Item& it, int base) __attribute__((always_inline)) -> uint32_t {
+    return base + lane < it.L ? a.col[it.beg + base + lane] : 0u;
+  };
+
+  bf16x8 qf[2][KS];
+  auto load_q = [&](const Item& it) __attribute__((always_inline)) {
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      const int row = min(it.qb * kBlk + 32 * nt + n, a.S_q - 1);
+      const __bf16* qp = a.q + (((size_t)it.b * a.Hq + it.h0 + wave) * a.S_q + row) * D + 8 * hf;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qp + 16 * ks);
+    }
+  };
+  // Q fragments are only MFMA operands: keep them in AGPRs (the VGPRs hold
+  // the softmax state, P and the LDS fragments)
+  auto q_to_agpr = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+a"(qf[nt][ks]));
+  };
+
+  f32x16 o[2][DT];
+  bf16x8 pa[2][4];  // P of one tile: [nt][chunk]
+  float m[2], l[2];
+#pragma unroll
+  for (int nt = 0; nt < 2; ++nt) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[nt][dt] = f32x16{};
+    m[nt] = -INFINITY;
+    l[nt] = 0.f;
+  }
+
+  const char* lds_bytes = (const char*)smem;
+  auto k_frag = [&](uint32_t kbase, int q) __attribute__((always_inline)) -> bf16x8 {  // q = 2*ks + sg
+    return *(const bf16x8*)(lds_bytes + kbase + (q & 1) * 32 * D * 2 + koff[q >> 1]);
+  };
+  auto v_frag = [&](uint32_t vbase, int q) __attribute__((always_inline)) -> bf16x8 {  // q = 4*chunk + dt
+    const int ch = q >> 2, dt = q & 3;
+    const char* base = lds_bytes + vbase + (32 * (ch >> 1) + 16 * (ch & 1)) * D * 2;
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[0][dt]));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[1][dt]));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  auto stage_bytes = [](int s) __attribute__((always_inline)) -> uint32_t { return (uint32_t)(2 * s) * TB; };
+
+  // ---- first item ----
+  int j = 0;  // round of the current item
+  Item cur, nxt;
+  if (!decode(j, cur)) return;
+  bool have_next = decode(j + 1, nxt);
+  int pos = 0;          // stream position of cur's tile 0
+  int issued_cur = 0;   // tiles of cur already copied
+  int issued_next = 0;  // tiles of nxt already copied
+  uint32_t win0 = load_entry_vec(cur, 0), win1 = load_entry_vec(cur, 64);
+  uint32_t nwin = have_next ? load_entry_vec(nxt, 0) : 0u;
+  load_q(cur);
+  asm volatile("" ::"v"(win0), "v"(win1), "v"(nwin));
+  q_to_agpr();
+  wait_vm<0>();
+  int wbase = 0;  // the window holds entries wbase .. wbase+127 of cur
+  auto entry = [&](int t) __attribute__((always_inline)) -> uint32_t {
+    const int off = t - wbase;
+    return (uint32_t)__builtin_amdgcn_readlane((int)(off < 64 ? win0 : win1), off & 63);
+  };
+
+  f32x16 sc[2][2];  // S of the current tile: [nt][sg]
+
+  while (true) {
+    const int L = cur.L;
+    // catch up on the copies of cur's first tiles that the previous item did
+    // not get to (its stream ended early, or this is the first item)
+    for (; issued_cur < min(L, ST - 2); ++issued_cur)
+      issue_tile(cur, (pos + issued_cur) % ST, (int)(entry(issued_cur) & 0x7fffffffu));
+    wait_vm<0>();
+    __syncthreads();
+
+    // S_t = K_t Q^T: 32 MFMAs, the K fragments read two ahead.  On a
+    // partial tile (Section IV-A case iii) the elements beyond the causal
+    // limit or the last key are then set to -inf (rare: the diagonal tile).
+    auto qk_phase = [&](int t) __attribute__((always_inline)) {
+      const uint32_t kbase = stage_bytes((pos + t) % ST);
+      bf16x8 kf[3];
+      kf[0] = k_frag(kbase, 0);
+      kf[1] = k_frag(kbase, 1);
+      static_for<32>([&](auto slot) __attribute__((always_inline)) {
+        constexpr int s = decltype(slot)::value;
+        constexpr int q = s >> 1, nt = s & 1;
+        if constexpr (nt == 0 && q + 2 < 16) kf[(q + 2) % 3] = k_frag(kbase, q + 2);
+        sc[nt][q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            kf[q % 3], qf[nt][q >> 1], q < 2 ? f32x16{} : sc[nt][q & 1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      const uint32_t cw = entry(t);
+      if (cw >> 31) {
+        const int kb = (int)(cw & 0x7fffffffu);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int lim_abs = min(a.causal ? cur.qb * kBlk + 32 * nt + n + a.delta : INT_MAX - kBlk,
+                                  a.S_k - 1);
+          const int lim = lim_abs - (kb * kBlk + 4 * hf);
+#pragma unroll
+          for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int off = 32 * sg + 8 * (r >> 2) + (r & 3);
+              const unsigned dead = (unsigned)((lim - off) >> 31);
+              sc[nt][sg][r] = __uint_as_float((dead & 0xff800000u) |
+                                              (~dead & __float_as_uint(sc[nt][sg][r])));
+            }
+        }
+      }
+    };
+
+    // Half of chunk (t, ch) of P = 2^(S c - m): 4 exponentials, rounded to
+    // bf16; the second half also adds the chunk's bf16 values to l.  The
+    // empty statement pins the chunk to its slot (without a use there the
+    // compiler sinks the exponentials below the MFMAs they overlap).
+    float msafe[2];
+    auto p_chunk = [&](auto tv, auto chv, auto hv) __attribute__((always_inline)) {
+      constexpr int t = decltype(tv)::value, ch = decltype(chv)::value, h = decltype(hv)::value;
+      constexpr int sg = ch >> 1, half = ch & 1;
+#pragma unroll
+      for (int e = 4 * h; e < 4 * h + 4; ++e)
+        pa[t][ch][e] = (__bf16)__builtin_amdgcn_exp2f(
+            __builtin_fmaf(sc[t][sg][8 * half + e], a.c, -msafe[t]));
+      if constexpr (h == 1) {
+        const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+        for (int e = 0; e < 8; e += 2)
+          l[t] = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{pa[t][ch][e], pa[t][ch][e + 1]}, ones,
+                                                 l[t], false);
+        asm volatile("" ::"v"(pa[t][ch]), "v"(l[t]));
+      }
+    };
+
+    // Softmax of S_i into P_i on the VALU, interleaved with O += V_{i-1}
+    // P_{i-1} on the matrix core when PV is set (every tile but the first).
+    // P has one buffer: the PV MFMAs of slots 8c .. 8c+7 read chunk c of
+    // P_{i-1}, so chunk c of P_i is written after them (chunks 0-2 here,
+    // chunk 3 by p_tail once the phase is over).
+    auto soft_phase = [&](int i, auto pv_flag) __attribute__((always_inline)) {
+      constexpr bool do_pv = decltype(pv_flag)::value != 0;
+      const uint32_t vbase = stage_bytes((pos + i + ST - 1) % ST) + TB;
+      float mx[2] = {-INFINITY, -INFINITY};
+      bf16x8 vf[3];
+      if constexpr (do_pv) {
+        vf[0] = v_frag(vbase, 0);
+        vf[1] = v_frag(vbase, 1);
+      }
+      bool grow = false;
+      float alpha[2] = {1.f, 1.f};
+      static_for<32>([&](auto slot) __attribute__((always_inline)) {
+        constexpr int s = decltype(slot)::value;
+        constexpr int q = s >> 1, nt = s & 1;
+        if constexpr (do_pv) {
+          if constexpr (nt == 0 && q + 2 < 16) vf[(q + 2) % 3] = v_frag(vbase, q + 2);
+          mfma_acc(o[nt][q & 3], vf[q % 3], pa[nt][q >> 2]);
+        }
+        if constexpr (s < 8) {
+          // slots 0..7: row maxima, 8 scores per slot (N-tile s/4)
+          constexpr int t = s >> 2, sg = (s >> 1) & 1, r0 = 8 * (s & 1);
+#pragma unroll
+          for (int r = r0; r < r0 + 8; ++r) mx[t] = fmaxf(mx[t], sc[t][sg][r]);
+          asm volatile("" ::"v"(mx[t]));
+        } else if constexpr (s == 8) {
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const float x = other_half_max(mx[t]);
+            mx[t] = x == -INFINITY ? -INFINITY : x * a.c;
+            grow |= mx[t] > m[t] + TAU;
+          }
+        } else if constexpr (s == 9) {
+          const bool any = __builtin_amdgcn_ballot_w64(grow) != 0;
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            if (any) {
+              const float mnew = fmaxf(m[t], mx[t]);
+              alpha[t] = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[t] - mnew);
+              l[t] *= alpha[t];
+              m[t] = mnew;
+            }
+            msafe[t] = m[t] == -INFINITY ? 0.f : m[t];
+          }
+          grow = any;
+        } else if constexpr (s >= 10 && s < 14) {
+          p_chunk(Par<((s - 10) >> 1)>{}, Par<0>{}, Par<((s - 10) & 1)>{});
+        } else if constexpr (s >= 16 && s < 20) {
+          p_chunk(Par<((s - 16) >> 1)>{}, Par<1>{}, Par<((s - 16) & 1)>{});
+        } else if constexpr (s >= 24 && s < 28) {
+          p_chunk(Par<((s - 24) >> 1)>{}, Par<2>{}, Par<((s - 24) & 1)>{});
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      // O holds sums relative to the old maxima: rescale before P_i enters it
+      // (rare: only when some row max grew by more than TAU; O is still 0 on
+      // the first tile)
+      if constexpr (do_pv) {
+        if (grow) {
+          // element by element through one VGPR each (O stays in AGPRs);
+          // the nops keep the reads clear of the last MFMA's write
+          asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+              for (int r = 0; r < 16; ++r) o[t][dt][r] = acc_write(acc_read(o[t][dt][r]) * alpha[t]);
+        }
+      }
+    };
+    // the last chunk of P_i, after every PV MFMA of the phase
+    auto p_tail = [&]() __attribute__((always_inline)) {
+      p_chunk(Par<0>{}, Par<3>{}, Par<0>{});
+      p_chunk(Par<0>{}, Par<3>{}, Par<1>{});
+      p_chunk(Par<1>{}, Par<3>{}, Par<0>{});
+      p_chunk(Par<1>{}, Par<3>{}, Par<1>{});
+    };
+
+    // copy of stream position pos + i + 3: tile i+3 of cur or a first tile
+    // of nxt; returns whether one was issued
+    auto copy_ahead = [&](int i) __attribute__((always_inline)) -> bool {
+      const int t3 = i + ST - 2;
+      const int cstage = (pos + t3) % ST;
+      if (t3 < L && t3 >= wbase + 128) {  // slide the window (once per 64 tiles)
+        wbase += 64;
+        win0 = win1;
+        win1 = load_entry_vec(cur, wbase + 64);
+        asm volatile("" ::"v"(win1));
+      }
+      const bool in_cur = t3 < L;
+      const bool in_next = !in_cur && have_next && t3 - L == issued_next && issued_next < nxt.L;
+      if (in_cur)
+        issue_tile(cur, cstage, (int)(entry(t3) & 0x7fffffffu));
+      else if (in_next)
+        issue_tile(nxt, cstage,
+                   (int)((uint32_t)__builtin_amdgcn_readlane((int)nwin, issued_next) & 0x7fffffffu));
+      // counters updated outside the branches (kept in SGPRs)
+      issued_cur += in_cur ? 1 : 0;
+      issued_next += in_next ? 1 : 0;
+      return in_cur || in_next;
+    };
+    // tile i+2 (read as K in the next iteration) must have landed: only the
+    // copy issued in this iteration may still be in flight
+    auto end_iteration = [&](bool copied) __attribute__((always_inline)) {
+      wait_vm_upto(copied ? CPT : 0);
+      __syncthreads();
+    };
+    // middle tile i (0 < i < L-1): softmax(i) with PV(i-1), then S_{i+1}
+    auto middle = [&](int i, auto) __attribute__((always_inline)) {
+      const bool copied = copy_ahead(i);
+      soft_phase(i, Par<1>{});
+      p_tail();
+      qk_phase(i + 1);
+      end_iteration(copied);
+    };
+
+    if (L > 0) {
+      qk_phase(0);
+      // tile 0: softmax only (O is still empty), then S_1
+      {
+        const bool copied = copy_ahead(0);
+        soft_phase(0, Par<0>{});
+        p_tail();
+        if (L > 1) qk_phase(1);
+        end_iteration(copied);
+      }
+      int i = 1;
+      for (; i + 1 < L; ++i) middle(i, Par<0>{});
+      // last tile i = L-1 (> 0): softmax(i) with PV(i-1), no further S
+      if (i == L - 1 && i > 0) {
+        const bool copied = copy_ahead(i);
+        soft_phase(i, Par<1>{});
+        p_tail();
+        end_iteration(copied);
+      }
+    }
+
+    // Next item: its Q rows are loaded now (qf is free: the last S was
+    // computed in iteration L-2), then O += V_{L-1} P_{L-1} and the output.
+    const bool more = have_next;
+    Item after;
+    bool have_after = false;
+    if (more) {
+      have_after = decode(j + 2, after);
+      load_q(nxt);
+    }
+    if (L > 0) {
+      const uint32_t vbase = stage_bytes((pos + L - 1) % ST) + TB;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const bf16x8 vf = v_frag(vbase, q);
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt)
+          mfma_acc(o[nt][q & 3], vf, pa[nt][q >> 2]);
+      }
+    }
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");  // O reads after the last MFMA
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int qrow = cur.qb * kBlk + 32 * t + n;
+      const float lt = half_pair_sum(l[t]);
+      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      if (qrow < a.S_q) {
+        float* op = a.out + (((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q + qrow) * D + 4 * hf;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int gq = 0; gq < 4; ++gq) {
+            f32x4 w = {acc_read(o[t][dt][4 * gq]) * inv, acc_read(o[t][dt][4 * gq + 1]) * inv,
+                       acc_read(o[t][dt][4 * gq + 2]) * inv, acc_read(o[t][dt][4 * gq + 3]) * inv};
+            *(f32x4*)(op + 32 * dt + 8 * gq) = w;
+          }
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][dt][r] = acc_write(0.f);
+      m[t] = -INFINITY;
+      l[t] = 0.f;
+    }
+    if (!more) break;
+    pos += L;
+    cur = nxt;
+    issued_cur = issued_next;
+    issued_next = 0;
+    have_next = have_after;
+    if (have_after) nxt = after;
+    j += 1;
+    wbase = 0;
+    win0 = nwin;
+    win1 = load_entry_vec(cur, 64);
+    nwin = have_next ? load_entry_vec(nxt, 0) : 0u;
+    asm volatile("" ::"v"(win0), "v"(win1), "v"(nwin));
+    q_to_agpr();
+  }
+}
+
+hipError_t launch_attention_w64(const AttnArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_attn_w64<128>, dim3(256), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace steel
