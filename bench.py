@@ -44,7 +44,8 @@ DEFAULT_WORKLOAD = "gqa32x8_s16384_d128_window1024_sink64"
 PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12     # 2516.6
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2607_09385_amd", "csrc", "attn_fwd.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_09385_amd", "csrc", f)
+               for f in ("attn_common.h", "attn_fwd.hip", "attn_w64.hip")]
 
 
 def live_tile_counts(mask, B, Hq, S_q, S_k, causal, blk=64):
@@ -62,8 +63,13 @@ def live_tile_counts(mask, B, Hq, S_q, S_k, causal, blk=64):
 
 
 def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the attention kernels' sources: counter readings taken on other
+    sources are not reported."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_for(workload):

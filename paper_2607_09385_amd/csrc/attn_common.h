@@ -88,7 +88,11 @@ __device__ __forceinline__ void copy16_to_lds(const void* sbase, uint32_t voff, 
   const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
   const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
   const uint64_t ps = (hi << 32) | lo;
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+  // The base comes from v_readfirstlane just before the statement: a VMEM
+  // instruction may read an SGPR only 5 wait states after a VALU wrote it,
+  // and the compiler pads only the instructions it emits itself, so the
+  // statement pads its own (s_mov + s_nop 4; also covers the M0 write).
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 4\n\tglobal_load_lds_dwordx4 %1, %2"
                :
                : "s"(__builtin_amdgcn_readfirstlane(lds_base)), "v"(voff), "s"(ps)
                : "memory", "m0");

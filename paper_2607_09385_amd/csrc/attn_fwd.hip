@@ -425,7 +425,8 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
     ap.order = w.order_p;
     ap.n_items = w.n_items + 1;
     if (p.pack == 2) launch_one<D, 2>(ap, p.NP, s);
-    else if (D == 128 && STEEL_W64) launch_attention_w64(ap, s);
+    else if (D == 128 && STEEL_W64 && (size_t)p.S_q * D * 4 < (1ull << 31))
+      launch_attention_w64(ap, s);
     else launch_one<D, 4>(ap, p.NP, s);
   }
   a.order = w.order_s;

@@ -7,18 +7,18 @@
 //
 // * Each wave owns all 64 rows of its head (two 32-row MFMA N-tiles), so
 //   every K or V fragment read from LDS feeds two MFMAs: half the LDS read
-//   traffic of 32-row waves.  One wave per SIMD; the MFMA accumulators (S of
-//   two tiles and O) live in AGPRs.
+//   traffic of 32-row waves.  One wave per SIMD; O and the Q fragments live
+//   in AGPRs (the O MFMAs are issued as inline assembly on AGPR
+//   accumulators), S in VGPRs where the softmax reads it.
 // * Software pipeline over the tiles i of an item: iteration i runs the
-//   softmax of S_i on the VALU while the matrix core computes S_{i+1} =
-//   K_{i+1} Q^T and O += V_{i-1} P_{i-1}.  The three streams are interleaved
-//   in 32 slots of two MFMAs each, so one wave keeps the matrix core and the
-//   VALU busy at the same time (the paper's three pipeline stages, Algorithm
-//   1, running concurrently inside one wavefront).
+//   softmax of S_i on the VALU while the matrix core computes O += V_{i-1}
+//   P_{i-1}, the two interleaved in 32 slots of one MFMA each, then
+//   S_{i+1} = K_{i+1} Q^T (the paper's pipeline stages, Algorithm 1, running
+//   concurrently inside one wavefront).
 // * K/V tiles flow through a 5-stage LDS ring (160 KiB) in one stream across
 //   the workgroup's items: while an item finishes, the first tiles of the
-//   next one are already being copied, and its Q rows are loaded during the
-//   last iteration.
+//   next one are already being copied, and its Q rows are loaded before
+//   the item's last O update.
 // * One workgroup per CU; each takes one item per round of its XCD's share
 //   of the work order (the same XCD-aware placement as k_attn), serpentine
 //   over rounds.
