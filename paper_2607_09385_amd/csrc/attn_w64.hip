@@ -481,29 +481,50 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
           mfma_acc(o[nt][q & 3], vf, pa[nt][q >> 2]);
       }
     }
+    // Output O / l, staged through LDS so that every store instruction
+    // writes two whole 512-byte rows (in the accumulator layout a lane holds
+    // 16-byte pieces of one row, and one store would touch 32 rows).  The
+    // stages of stream positions pos+L+3 and pos+L+4 are free here: the
+    // first was last read in iteration L-2, the second (tile L-1) once every
+    // wave has done the O update above, and neither is refilled before the
+    // next item's first barrier.  Each wave stages 32 rows (16 KiB) at a
+    // time, 16-byte chunk c of row r at chunk c ^ r (conflict-free both
+    // ways); it reads back only what it wrote, so no barrier separates the
+    // two halves.
+    __syncthreads();
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7");  // O reads after the last MFMA
+    {
+      char* const stg = (char*)smem + stage_bytes((pos + L + 3 + (wave >> 1)) % ST) +
+                        (uint32_t)(wave & 1) * 16384u;
+      float* const ob = a.out + ((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q * D;
+      const int rr = lane >> 5, cc = lane & 31;  // read-back: row 2k + rr, chunk cc
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int qrow = cur.qb * kBlk + 32 * t + n;
-      const float lt = half_pair_sum(l[t]);
-      const float inv = lt > 0.f ? 1.f / lt : 0.f;
-      if (qrow < a.S_q) {
-        float* op = a.out + (((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q + qrow) * D + 4 * hf;
+      for (int t = 0; t < 2; ++t) {
+        const float lt = half_pair_sum(l[t]);
+        const float inv = lt > 0.f ? 1.f / lt : 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
           for (int gq = 0; gq < 4; ++gq) {
-            f32x4 w = {acc_read(o[t][dt][4 * gq]) * inv, acc_read(o[t][dt][4 * gq + 1]) * inv,
-                       acc_read(o[t][dt][4 * gq + 2]) * inv, acc_read(o[t][dt][4 * gq + 3]) * inv};
-            *(f32x4*)(op + 32 * dt + 8 * gq) = w;
+            const f32x4 w = {acc_read(o[t][dt][4 * gq]) * inv, acc_read(o[t][dt][4 * gq + 1]) * inv,
+                             acc_read(o[t][dt][4 * gq + 2]) * inv, acc_read(o[t][dt][4 * gq + 3]) * inv};
+            const int chunk = 8 * dt + 2 * gq + hf;  // columns 4 * chunk .. 4 * chunk + 3 of row n
+            *(f32x4*)(stg + n * 512 + ((chunk ^ n) << 4)) = w;
           }
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+          const int r = 2 * k + rr;
+          const f32x4 w = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
+          const int qrow = cur.qb * kBlk + 32 * t + r;
+          if (qrow < a.S_q) *(f32x4*)(ob + (size_t)qrow * D + 4 * cc) = w;
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[t][dt][r] = acc_write(0.f);
+        m[t] = -INFINITY;
+        l[t] = 0.f;
       }
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[t][dt][r] = acc_write(0.f);
-      m[t] = -INFINITY;
-      l[t] = 0.f;
     }
     if (!more) break;
     pos += L;

@@ -64,6 +64,7 @@ SMALL = [
     ("sq_lt_sk", 1, 4, 2, 100, 300, 128, True, "random"),
     ("sq_gt_sk_dead_rows", 1, 2, 1, 300, 100, 64, True, "none"),
     ("gqa8_uniform_mask", 1, 8, 1, 256, 256, 128, True, "uniform"),
+    ("gqa4_packs_ragged_d128", 2, 8, 2, 200, 200, 128, True, "none"),
     ("gqa4_random_mask", 2, 8, 2, 320, 320, 64, True, "random"),
     ("gqa2_mixed_packs", 1, 4, 2, 384, 384, 128, True, "mixed"),
     ("dead_query_blocks", 1, 4, 4, 256, 256, 64, False, "deadrows"),
