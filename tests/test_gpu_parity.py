@@ -65,6 +65,12 @@ SMALL = [
     ("sq_gt_sk_dead_rows", 1, 2, 1, 300, 100, 64, True, "none"),
     ("gqa8_uniform_mask", 1, 8, 1, 256, 256, 128, True, "uniform"),
     ("gqa4_packs_ragged_d128", 2, 8, 2, 200, 200, 128, True, "none"),
+    # more head-pack items than the packed kernel's 256 persistent
+    # workgroups: each takes two or three, so item transitions (next item's
+    # first tiles and Q rows, output staging) are checked against the full
+    # oracle; the uniform mask mixes items with 0, 1, 2 and more live tiles
+    ("packs_multi_item_causal", 8, 32, 8, 512, 512, 128, True, "none"),
+    ("packs_multi_item_masked_ragged", 8, 32, 8, 600, 600, 128, True, "uniform"),
     ("gqa4_random_mask", 2, 8, 2, 320, 320, 64, True, "random"),
     ("gqa2_mixed_packs", 1, 4, 2, 384, 384, 128, True, "mixed"),
     ("dead_query_blocks", 1, 4, 4, 256, 256, 64, False, "deadrows"),
