@@ -76,6 +76,31 @@ __device__ __forceinline__ float acc_write(float v) {
 // softmax), the output accumulator stays in AGPRs: it is only read by the
 // rescale and the epilogue, through acc_read after explicit waits.  In-place
 // accumulation chains are at least 8 MFMAs apart.
+// Four 16-byte global -> LDS copies per lane from one SGPR base: copy j
+// writes LDS bytes [lds + 1024 j + 16 lane, +16) from base + off_j.  The
+// nops: 5 wait states between a VALU write of an SGPR the copies read and
+// the first copy (the compiler pads only its own instructions), and 1 after
+// each M0 write.
+__device__ __forceinline__ void copy4_to_lds(uint64_t base, uint32_t lds, uint32_t o0, uint32_t o1,
+                                             uint32_t o2, uint32_t o3) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 4\n\t"
+      "global_load_lds_dwordx4 %2, %1\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %3, %1\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %4, %1\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %5, %1"
+      :
+      : "s"(lds), "s"(base), "v"(o0), "v"(o1), "v"(o2), "v"(o3)
+      : "memory", "m0", "scc");
+}
+
 __device__ __forceinline__ void mfma_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
@@ -104,7 +129,8 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
     return;  // index was planned for another problem: leave out untouched
   const int n_all = ((cint_p)a.n_items)[0];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // in an SGPR
   const int n = lane & 31, hf = lane >> 5;
   const int xb = (int)blockIdx.x & 7, wb = (int)blockIdx.x >> 3, nwb = (int)gridDim.x >> 3;
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(smem));
@@ -162,12 +188,17 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
     return true;
   };
 
+  // this lane's byte offsets of its four 16-byte chunks of a tile
+  static_assert(LPW == 4, "four copies per lane, tile and tensor");
+  const uint32_t co0 = cp_off(0), co1 = cp_off(1), co2 = cp_off(2), co3 = cp_off(3);
   auto issue_copy = [&](const __bf16* src, uint32_t dst, int kb) __attribute__((always_inline)) {
     const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW) * 1024u;
     if ((kb + 1) * kBlk <= a.S_k) {
-      const __bf16* sb = src + (size_t)kb * kBlk * D;
-#pragma unroll
-      for (int j = 0; j < LPW; ++j) copy16_to_lds(sb, cp_off(j), lbase + j * 1024u);
+      // the item's pointers may sit in VGPRs: the base goes to an SGPR pair
+      const uint64_t p = (uint64_t)(uintptr_t)(src + (size_t)kb * kBlk * D);
+      const uint64_t ps = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
+                          (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+      copy4_to_lds(ps, __builtin_amdgcn_readfirstlane(lbase), co0, co1, co2, co3);
     } else {
 #pragma unroll
       for (int j = 0; j < LPW; ++j) {
