@@ -165,23 +165,57 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
     const __bf16* kg;
     const __bf16* vg;
   };
-  // The k-th item of this workgroup is position j of its XCD's share of the
-  // work order, j = k*nwb + w for even k and k*nwb + (nwb-1-w) for odd k
-  // (serpentine): the share is sorted heaviest first, so a workgroup that
-  // takes a heavy item in one round takes a light one in the next.
+  // This workgroup's items: in round r it takes position
+  // r*nwb + w (even r) or r*nwb + (nwb-1-w) (odd r) of its XCD's share of the
+  // work order (serpentine: the share is sorted heaviest first, so a
+  // workgroup that takes a heavy item in one round takes a light one in the
+  // next).  It runs its rounds in the order K-1, 0, 1, ..., K-2: the same
+  // items, but the lightest round first, so that workgroups whose items all
+  // have the same length do not all reach their item boundaries (Q loads,
+  // output stores) at the same moment.
+  const int n_x = (n_all / (8 * kXcdGroup)) * kXcdGroup +
+                  min(max(n_all % (8 * kXcdGroup) - kXcdGroup * xb, 0), kXcdGroup);
+  const int K = (n_x + nwb - 1) / nwb;  // rounds of this XCD
+  auto round_pos = [&](int k) __attribute__((always_inline)) -> int {  // -1: none
+    if (k >= K) return -1;
+    const int r = k == 0 ? K - 1 : k - 1;
+    const int p = r * nwb + ((r & 1) ? nwb - 1 - wb : wb);
+    return p < n_x ? p : -1;
+  };
+  // The items are fetched 64 at a time with vector loads: lane t of w_item,
+  // w_beg, w_end holds item 64*iw + t (-1 if none) and the bounds of its
+  // live list, so decoding an item at an item boundary is register work
+  // (scalar loads there would share their wait counter with the LDS reads
+  // of the last O update and stall it).
+  int iw = -1;
+  int w_item = -1, w_beg = 0, w_end = 0;
+  auto load_items = [&](int win) __attribute__((always_inline)) {
+    const int p = round_pos(64 * win + lane);
+    const int idx = p < 0 ? n_all : xcd_slot(8 * p + xb);
+    w_item = -1;
+    w_beg = 0;
+    w_end = 0;
+    if (idx < n_all) {
+      w_item = a.order[idx];
+      const int r0 = (w_item / a.nQB) * 4 * a.nQB + w_item % a.nQB;
+      w_beg = a.row_ptr[r0];
+      w_end = a.row_ptr[r0 + 1];
+    }
+    // wait here (once per 64 items), not at every later use
+    asm volatile("" ::"v"(w_item), "v"(w_beg), "v"(w_end));
+    iw = win;
+  };
   auto decode = [&](int k, Item& it) __attribute__((always_inline)) -> bool {
-    const int j = k * nwb + ((k & 1) ? nwb - 1 - wb : wb);
-    const int idx = xcd_slot(8 * j + xb);
-    if (idx >= n_all) return false;
-    const int item = ((cint_p)a.order)[idx];
+    if ((k >> 6) != iw) load_items(k >> 6);
+    const int item = __builtin_amdgcn_readlane(w_item, k & 63);
+    if (item < 0) return false;
     it.qb = item % a.nQB;
     const int bh0 = (item / a.nQB) * 4;
     it.b = bh0 / a.Hq;
     const int h0 = bh0 % a.Hq;
     it.h0 = h0;
-    const int r0 = bh0 * a.nQB + it.qb;
-    it.beg = ((cint_p)a.row_ptr)[r0];
-    it.L = ((cint_p)a.row_ptr)[r0 + 1] - it.beg;
+    it.beg = __builtin_amdgcn_readlane(w_beg, k & 63);
+    it.L = __builtin_amdgcn_readlane(w_end, k & 63) - it.beg;
     const size_t kvoff = ((size_t)it.b * a.Hkv + h0 / a.G) * a.S_k * D;
     it.kg = a.k + kvoff;
     it.vg = a.v + kvoff;
@@ -264,7 +298,10 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   // ---- first item ----
   int j = 0;  // round of the current item
   Item cur, nxt;
-  if (!decode(j, cur)) return;
+  if (!decode(j, cur)) {  // no item in the lightest round: start with the next
+    j = 1;
+    if (!decode(j, cur)) return;
+  }
   bool have_next = decode(j + 1, nxt);
   int pos = 0;          // stream position of cur's tile 0
   int issued_cur = 0;   // tiles of cur already copied
@@ -495,22 +532,31 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
 
     // Next item: its Q rows are loaded now (qf is free: the last S was
     // computed in iteration L-2), then O += V_{L-1} P_{L-1} and the output.
+    // The live-list windows of the next two items are loaded here too,
+    // ahead of the output stores, so that waiting for them does not wait
+    // for the stores.
     const bool more = have_next;
     Item after;
     bool have_after = false;
+    uint32_t win1_next = 0u, nwin_next = 0u;
     if (more) {
       have_after = decode(j + 2, after);
       load_q(nxt);
+      win1_next = load_entry_vec(nxt, 64);
+      nwin_next = have_after ? load_entry_vec(after, 0) : 0u;
     }
     if (L > 0) {
+      // V fragments read two ahead, as in the soft phase
       const uint32_t vbase = stage_bytes((pos + L - 1) % ST) + TB;
+      bf16x8 vf[3];
+      vf[0] = v_frag(vbase, 0);
+      vf[1] = v_frag(vbase, 1);
+      static_for<16>([&](auto qv) __attribute__((always_inline)) {
+        constexpr int q = decltype(qv)::value;
+        if constexpr (q + 2 < 16) vf[(q + 2) % 3] = v_frag(vbase, q + 2);
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const bf16x8 vf = v_frag(vbase, q);
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-          mfma_acc(o[nt][q & 3], vf, pa[nt][q >> 2]);
-      }
+        for (int nt = 0; nt < 2; ++nt) mfma_acc(o[nt][q & 3], vf[q % 3], pa[nt][q >> 2]);
+      });
     }
     // Output O / l, staged through LDS so that every store instruction
     // writes two whole 512-byte rows (in the accumulator layout a lane holds
@@ -542,12 +588,24 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
             const int chunk = 8 * dt + 2 * gq + hf;  // columns 4 * chunk .. 4 * chunk + 3 of row n
             *(f32x4*)(stg + n * 512 + ((chunk ^ n) << 4)) = w;
           }
+        const int qrow0 = cur.qb * kBlk + 32 * t;
+        if (qrow0 + 32 <= a.S_q) {
+          // every row exists: all 16 reads first, then the stores
+          f32x4 w[16];
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
-          const int r = 2 * k + rr;
-          const f32x4 w = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
-          const int qrow = cur.qb * kBlk + 32 * t + r;
-          if (qrow < a.S_q) *(f32x4*)(ob + (size_t)qrow * D + 4 * cc) = w;
+          for (int k = 0; k < 16; ++k) {
+            const int r = 2 * k + rr;
+            w[k] = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
+          }
+#pragma unroll
+          for (int k = 0; k < 16; ++k) *(f32x4*)(ob + (size_t)(qrow0 + 2 * k + rr) * D + 4 * cc) = w[k];
+        } else {
+#pragma unroll
+          for (int k = 0; k < 16; ++k) {
+            const int r = 2 * k + rr;
+            const f32x4 w = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
+            if (qrow0 + r < a.S_q) *(f32x4*)(ob + (size_t)(qrow0 + r) * D + 4 * cc) = w;
+          }
         }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
@@ -567,8 +625,8 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
     j += 1;
     wbase = 0;
     win0 = nwin;
-    win1 = load_entry_vec(cur, 64);
-    nwin = have_next ? load_entry_vec(nxt, 0) : 0u;
+    win1 = win1_next;
+    nwin = nwin_next;
     asm volatile("" ::"v"(win0), "v"(win1), "v"(nwin));
     q_to_agpr();
   }
