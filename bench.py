@@ -281,7 +281,7 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_TFLOPS, 4),
             "traffic": traffic,
-            "kernel": "attention run (k_attn), index prebuilt",
+            "kernel": "attention run (k_attn_w64 for uniform head packs of 4 at D=128, k_attn for the other items), index prebuilt",
             "run_us": round(run_s * 1e6, 2),
             "algorithmic_flops_per_run": f_live,
         },
