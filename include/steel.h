@@ -132,6 +132,35 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out,
                    float scale, int causal, const void* workspace, size_t workspace_bytes,
                    void* stream);
 
+/*
+ * Structured-mask forms: the block mask is generated from block coordinates
+ * instead of read from a tensor (the paper builds masks on the core rather
+ * than fetching them, Section III-B, and names windowed attention among the
+ * masking schemes its coordinate tracking covers, Section IV-A).  Block
+ * (qb, kb) is in the mask iff
+ *     qb - window_blocks < kb <= qb      (window ending at the block diagonal)
+ *  or kb < sink_blocks                   (sink blocks at the start)
+ * and the causal structure is then applied exactly as for a mask tensor.  The
+ * result equals steel_attn_fwd / steel_attn_plan given that mask as a
+ * [B][Hq][nQB][nKB] tensor; no mask is read.  Every query head shares the
+ * pattern, so head packs always run together.
+ *
+ *   window_blocks  >= 1 (STEEL_ERR_INVALID_ARGUMENT otherwise)
+ *   sink_blocks    >= 0
+ *
+ * All other arguments, the workspace (same size as for steel_attn_plan),
+ * ownership and error behaviour are those of steel_attn_fwd and
+ * steel_attn_plan; a window plan is run with steel_attn_run.
+ */
+int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out,
+                          int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                          float scale, int causal, int window_blocks, int sink_blocks,
+                          void* stream);
+
+int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
+                           int window_blocks, int sink_blocks, void* workspace,
+                           size_t workspace_bytes, void* stream);
+
 /* Text of the last non-OK status returned on the calling thread ("" if none). */
 const char* steel_last_error(void);
 

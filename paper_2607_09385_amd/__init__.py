@@ -87,6 +87,36 @@ def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal:
     return out
 
 
+def attn_fwd_window(q, k, v, window_blocks: int, sink_blocks: int = 0, *,
+                    scale: Optional[float] = None, causal: bool = True, blk: int = BLK, out=None,
+                    stream=None):
+    """``attn_fwd`` with the block mask generated from coordinates: block
+    (qb, kb) is live iff qb - window_blocks < kb <= qb or kb < sink_blocks
+    (then causal as usual); no mask tensor is read."""
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_bf16(name, t)
+    B, Hq, S_q, D = q.shape
+    Bk, Hkv, S_k, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Bk != B or Dk != D:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    if q.device != k.device or q.device != v.device:
+        raise ValueError("q, k and v must be on the same device")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if out is None:
+        out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+    elif out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+    with torch.cuda.device(q.device):
+        st = _lib.load().steel_attn_fwd_window(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, Hq, Hkv, S_q, S_k, D, blk,
+            float(scale), 1 if causal else 0, int(window_blocks), int(sink_blocks),
+            _stream_handle(stream))
+    _lib.check(st)
+    return out
+
+
 def block_index(block_mask, B: int, Hq: int, S_q: int, S_k: int, *, causal: bool = True,
                 blk: int = BLK, device=None, stream=None):
     """Live-block list: returns (row_ptr int32 [R+1], col int32 [R*nKB]
@@ -115,10 +145,12 @@ def block_index(block_mask, B: int, Hq: int, S_q: int, S_k: int, *, causal: bool
 
 class Plan:
     """Live-block index built once for a mask and reused by ``run`` (the
-    two-phase form of ``attn_fwd``)."""
+    two-phase form of ``attn_fwd``).  ``window=(window_blocks, sink_blocks)``
+    plans the structured mask of ``attn_fwd_window`` instead (block_mask must
+    then be None)."""
 
     def __init__(self, block_mask, B: int, Hq: int, Hkv: int, S_q: int, S_k: int, *,
-                 causal: bool = True, blk: int = BLK, device=None, stream=None):
+                 causal: bool = True, blk: int = BLK, device=None, stream=None, window=None):
         torch = _torch()
         lib = _lib.load()
         nbytes = lib.steel_attn_workspace_bytes(B, Hq, Hkv, S_q, S_k, blk)
@@ -136,9 +168,17 @@ class Plan:
         self.causal, self.blk, self.device = bool(causal), blk, device
         self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         with torch.cuda.device(device):
-            st = lib.steel_attn_plan(None if block_mask is None else block_mask.data_ptr(),
-                                     B, Hq, Hkv, S_q, S_k, blk, 1 if causal else 0,
-                                     self.workspace.data_ptr(), nbytes, _stream_handle(stream))
+            if window is not None:
+                if block_mask is not None:
+                    raise ValueError("pass either block_mask or window, not both")
+                wb, sb = window
+                st = lib.steel_attn_plan_window(B, Hq, Hkv, S_q, S_k, blk, 1 if causal else 0,
+                                                int(wb), int(sb), self.workspace.data_ptr(), nbytes,
+                                                _stream_handle(stream))
+            else:
+                st = lib.steel_attn_plan(None if block_mask is None else block_mask.data_ptr(),
+                                         B, Hq, Hkv, S_q, S_k, blk, 1 if causal else 0,
+                                         self.workspace.data_ptr(), nbytes, _stream_handle(stream))
         _lib.check(st)
 
     def run(self, q, k, v, *, scale: Optional[float] = None, out=None, stream=None):

@@ -53,6 +53,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_attn_run.restype = c_int
     lib.steel_attn_run.argtypes = [c_void_p] * 4 + [c_int] * 7 + [c_float, c_int, c_void_p,
                                                                   c_size_t, c_void_p]
+    lib.steel_attn_fwd_window.restype = c_int
+    lib.steel_attn_fwd_window.argtypes = [c_void_p] * 4 + [c_int] * 7 + [c_float, c_int, c_int,
+                                                                         c_int, c_void_p]
+    lib.steel_attn_plan_window.restype = c_int
+    lib.steel_attn_plan_window.argtypes = [c_int] * 9 + [c_void_p, c_size_t, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

@@ -35,11 +35,23 @@ __device__ __forceinline__ bool partial_tile(const Problem& p, int qb, int kb) {
 
 // Live bits of tiles (qb, kb0 .. kb0+3) of one row (bit e = tile kb0 + e).
 // wide: the row holds whole 4-byte words (nKB % 4 == 0, aligned mask).
+// Without a mask tensor every block is in the mask, or, in the structured
+// mode (p.win_blocks > 0), the window and sink blocks of the coordinates.
 __device__ __forceinline__ uint32_t live_quad(const Problem& p, const uint8_t* mrow, bool wide,
                                               int qb, int kb0) {
   uint32_t bytes;
   if (mrow == nullptr) {
-    bytes = 0x01010101u;
+    if (p.win_blocks > 0) {
+      bytes = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int kb = kb0 + e;
+        const bool in = (kb <= qb && kb > qb - p.win_blocks) || kb < p.sink_blocks;
+        bytes |= (uint32_t)in << (8 * e);
+      }
+    } else {
+      bytes = 0x01010101u;
+    }
   } else if (wide) {
     bytes = kb0 < p.nKB ? *(const uint32_t*)(mrow + kb0) : 0u;
   } else {

@@ -30,6 +30,13 @@ struct Problem {
   int delta;    // S_k - S_q
   int R;        // B*Hq*nQB rows of the live-block list
   int NP;       // B*(Hq/pack)*nQB head packs (0 when pack == 1)
+  // Block mask from coordinates instead of a mask tensor (win_blocks > 0):
+  // block (qb, kb) is in the mask iff qb - win_blocks < kb <= qb (a window
+  // of win_blocks blocks ending at the block diagonal) or kb < sink_blocks.
+  // The index kernels then read no mask (the paper generates masks on the
+  // core rather than fetching them, Section III-B; windowed attention is the
+  // masking scheme Section IV-A names).
+  int win_blocks, sink_blocks;
 };
 
 // Device workspace of one call.

@@ -160,6 +160,18 @@ void set_pack(steel::Problem* p) {
   p->NP = p->pack > 1 ? p->R / p->pack : 0;
 }
 
+// Structured mask (window of window_blocks blocks ending at the block
+// diagonal, plus the first sink_blocks key blocks) in place of a mask tensor.
+int set_window(steel::Problem* p, int window_blocks, int sink_blocks) {
+  if (window_blocks < 1)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "window_blocks must be >= 1 (got %d)", window_blocks);
+  if (sink_blocks < 0)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "sink_blocks must be >= 0 (got %d)", sink_blocks);
+  p->win_blocks = window_blocks;
+  p->sink_blocks = sink_blocks;
+  return STEEL_OK;
+}
+
 steel::IndexBuffers carve(char* ws, const Layout& L) {
   steel::IndexBuffers w;
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
@@ -183,23 +195,11 @@ int check_workspace(const void* ws, size_t bytes, const Layout& L) {
   return STEEL_OK;
 }
 
-}  // namespace
-
-extern "C" {
-
-const char* steel_version(void) { return "libsteel 0.1.0 (gfx950)"; }
-
-const char* steel_last_error(void) { return g_err.c_str(); }
-
-int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* block_mask,
-                   void* out, int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
-                   float scale, int causal, void* stream) {
-  g_err.clear();
-  steel::Problem p{};
-  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
-  if (rc != STEEL_OK) return rc;
-  set_pack(&p);
-
+// The fused call once the arguments are checked: stream-ordered workspace,
+// index build, attention, workspace release.
+int fused_call(const steel::Problem& p, const void* q, const void* k, const void* v,
+               const uint8_t* block_mask, void* out, float scale, void* stream) {
+  int rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
@@ -220,6 +220,37 @@ int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* b
   return STEEL_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+const char* steel_version(void) { return "libsteel 0.1.0 (gfx950)"; }
+
+const char* steel_last_error(void) { return g_err.c_str(); }
+
+int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* block_mask,
+                   void* out, int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                   float scale, int causal, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  set_pack(&p);
+  return fused_call(p, q, k, v, block_mask, out, scale, stream);
+}
+
+int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out, int B, int Hq,
+                          int Hkv, int S_q, int S_k, int D, int blk, float scale, int causal,
+                          int window_blocks, int sink_blocks, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  if ((rc = set_window(&p, window_blocks, sink_blocks)) != STEEL_OK) return rc;
+  set_pack(&p);
+  return fused_call(p, q, k, v, nullptr, out, scale, stream);
+}
+
 size_t steel_attn_workspace_bytes(int B, int Hq, int Hkv, int S_q, int S_k, int blk) {
   g_err.clear();
   steel::Problem p{};
@@ -238,6 +269,23 @@ int steel_attn_plan(const uint8_t* block_mask, int B, int Hq, int Hkv, int S_q, 
   const Layout L = layout(p, true);
   if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
   hipError_t e = steel::launch_block_index(p, block_mask, carve(static_cast<char*>(workspace), L),
+                                           static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "launching the index build");
+  return STEEL_OK;
+}
+
+int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
+                           int window_blocks, int sink_blocks, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  if ((rc = set_window(&p, window_blocks, sink_blocks)) != STEEL_OK) return rc;
+  set_pack(&p);
+  const Layout L = layout(p, true);
+  if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
+  hipError_t e = steel::launch_block_index(p, nullptr, carve(static_cast<char*>(workspace), L),
                                            static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "launching the index build");
   return STEEL_OK;

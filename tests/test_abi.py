@@ -129,3 +129,20 @@ def test_workspace_bytes_and_plan_run_checks():
     st = lib.steel_attn_run(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.1, 1, FAKE, 16,
                             None)
     assert st == 1 and "smaller" in _lib.last_error()
+
+
+def test_window_forms_reject_invalid_window():
+    lib = _lib.load()
+    need = lib.steel_attn_workspace_bytes(1, 4, 2, 128, 128, 64)
+    st = lib.steel_attn_plan_window(1, 4, 2, 128, 128, 64, 1, 0, 1, FAKE, need, None)
+    assert st == 1 and "window_blocks" in _lib.last_error()
+    st = lib.steel_attn_plan_window(1, 4, 2, 128, 128, 64, 1, 2, -1, FAKE, need, None)
+    assert st == 1 and "sink_blocks" in _lib.last_error()
+    st = lib.steel_attn_plan_window(1, 4, 2, 128, 128, 64, 1, 2, 1, FAKE, need - 1, None)
+    assert st == 1 and "smaller" in _lib.last_error()
+    st = lib.steel_attn_fwd_window(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.125, 1,
+                                   0, 0, None)
+    assert st == 1 and "window_blocks" in _lib.last_error()
+    st = lib.steel_attn_fwd_window(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 96, 64, 0.125, 1,
+                                   2, 0, None)
+    assert st == 2 and "D=96" in _lib.last_error()
