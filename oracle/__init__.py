@@ -12,7 +12,9 @@ It is written from the paper's definitions, independently of the GPU code:
 * ``block_index`` -- the tile classification of Section IV-A (a tile is
   skipped, processed as is, or masked locally), written as a compressed
   per-query-block list, plus the heaviest-first work order that stands in for
-  the sparsity-aware placement of Section IV-C.
+  the sparsity-aware placement of Section IV-C;
+* ``block_select`` -- the mask producer that runs before the pass: top-k key
+  blocks per query block by mean-pooled query/key score, plus the diagonal.
 
 Every function is pinned by tests against things other than itself: brute
 force on tiny inputs, closed forms, invariants and an independent library
@@ -20,3 +22,4 @@ routine (see the module docstrings).
 """
 from .masked_attention import attention, attention_rows, element_visibility, kv_head  # noqa: F401
 from .block_index import N_BINS, build_index, count_bin, tile_classes, work_order  # noqa: F401
+from .block_select import block_means, block_scores, keep_count, topk_meanpool_mask  # noqa: F401
