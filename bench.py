@@ -304,8 +304,34 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
             "algorithmic_flops_per_run": f_live,
         },
     }
+    # top-k workloads: the mask producer that precedes the pass, on the device
+    producer = None
+    if cfg.mask == "topk_meanpool":
+        mask_dev = torch.empty((cfg.B, cfg.Hq, cfg.nQB, cfg.nKB), dtype=torch.uint8, device=dev)
+
+        def step_m():
+            steel.topk_block_mask(qd, kd, 1, 10, causal=cfg.causal, out=mask_dev)
+        for _ in range(warmup):
+            step_m()
+        e0.record(stream)
+        for _ in range(steps):
+            step_m()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_m = e0.elapsed_time(e1) / 1e3 / steps
+        same = bool(torch.equal(mask_dev.cpu(), torch.from_numpy(mask)))
+        # algorithmic bytes: Q and K read once, the mask written once
+        nbytes = 2 * (q.numel() + k.numel()) + mask_dev.numel()
+        producer = {"call": "steel_topk_block_mask", "us": round(t_m * 1e6, 2),
+                    "equals_workload_mask": same,
+                    "roofline": {"bound": "hbm", "achieved": round(nbytes / t_m / 1e9, 1),
+                                 "peak": 8000.0, "unit": "GB/s",
+                                 "frac": round(nbytes / t_m / 1e9 / 8000.0, 4),
+                                 "algorithmic_bytes": nbytes}}
     if structured is not None:
         line["structured_mask"] = structured
+    if producer is not None:
+        line["mask_producer"] = producer
     if want_cpu:
         print(f"[bench] {name}: CPU oracle baseline (~{cpu_seconds}s)", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(cfg, q, k, v, mask, counts, cpu_seconds)

@@ -161,6 +161,39 @@ int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, in
                            int window_blocks, int sink_blocks, void* workspace,
                            size_t workspace_bytes, void* stream);
 
+/*
+ * Block-mask producer run ahead of the pass: top-k key blocks per query block
+ * by mean-pooled score, plus the diagonal block.  (The paper generates masks
+ * on the compute core rather than fetching them, Section III-B, and any block
+ * mask then goes through the tile classes of Section IV-A.)  For every
+ * (b, query head h, query block qb), with g = h / (Hq/Hkv):
+ *   mean_q(qb)  float64 mean of the block's rows of Q[b][h] (a ragged last
+ *               block averages the rows it has); mean_k(kb) likewise of
+ *               K[b][g]
+ *   score(kb)   dot(mean_q(qb), mean_k(kb)) in float64
+ *   candidates  kb < min(qb + 1, nKB) when causal, kb < nKB otherwise
+ *   kept        the ceil(keep_num / keep_den * #candidates) candidates with
+ *               the largest scores (equal scores: the smaller kb first), and
+ *               kb = qb when qb < nKB
+ * block_mask[b][h][qb][kb] = 1 for kept blocks and 0 for all others (every
+ * byte of the [B][Hq][nQB][nKB] mask is written).  The float64 operation
+ * order is fixed (rows summed in increasing order, mean = sum / row count,
+ * products summed in increasing d without fused multiply-add), so the mask is
+ * reproducible bit for bit.
+ *
+ *   q, k        bf16 device tensors laid out as for steel_attn_fwd
+ *   D           64 or 128; blk 64; nKB <= 4096 (STEEL_ERR_UNSUPPORTED)
+ *   keep_num, keep_den   1 <= keep_num <= keep_den (1 and 10: 10%)
+ *   block_mask  uint8 device buffer of B*Hq*nQB*nKB bytes, caller-owned
+ *
+ * Float64 workspace for the block means and scores is taken stream-ordered
+ * from the per-device pool and released stream-ordered; the call only
+ * enqueues.  Errors as for steel_attn_fwd.
+ */
+int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, int S_q,
+                          int S_k, int D, int blk, int causal, int keep_num, int keep_den,
+                          uint8_t* block_mask, void* stream);
+
 /* Text of the last non-OK status returned on the calling thread ("" if none). */
 const char* steel_last_error(void);
 

@@ -117,6 +117,31 @@ def attn_fwd_window(q, k, v, window_blocks: int, sink_blocks: int = 0, *,
     return out
 
 
+def topk_block_mask(q, k, keep_num: int = 1, keep_den: int = 10, *, causal: bool = True,
+                    blk: int = BLK, out=None, stream=None):
+    """Block mask uint8 [B, Hq, nQB, nKB]: per query block the top
+    ceil(keep_num/keep_den * candidates) key blocks by mean-pooled q.k score
+    (ties to the smaller block), plus the diagonal block; computed on the GPU."""
+    torch = _torch()
+    _check_bf16("q", q)
+    _check_bf16("k", k)
+    B, Hq, S_q, D = q.shape
+    Bk, Hkv, S_k, Dk = k.shape
+    if Bk != B or Dk != D:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)}")
+    nQB, nKB = -(-S_q // blk), -(-S_k // blk)
+    if out is None:
+        out = torch.empty((B, Hq, nQB, nKB), dtype=torch.uint8, device=q.device)
+    elif out.dtype != torch.uint8 or tuple(out.shape) != (B, Hq, nQB, nKB) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous uint8 tensor [{B}, {Hq}, {nQB}, {nKB}]")
+    with torch.cuda.device(q.device):
+        st = _lib.load().steel_topk_block_mask(
+            q.data_ptr(), k.data_ptr(), B, Hq, Hkv, S_q, S_k, D, blk, 1 if causal else 0,
+            int(keep_num), int(keep_den), out.data_ptr(), _stream_handle(stream))
+    _lib.check(st)
+    return out
+
+
 def block_index(block_mask, B: int, Hq: int, S_q: int, S_k: int, *, causal: bool = True,
                 blk: int = BLK, device=None, stream=None):
     """Live-block list: returns (row_ptr int32 [R+1], col int32 [R*nKB]

@@ -58,6 +58,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                                          c_int, c_void_p]
     lib.steel_attn_plan_window.restype = c_int
     lib.steel_attn_plan_window.argtypes = [c_int] * 9 + [c_void_p, c_size_t, c_void_p]
+    lib.steel_topk_block_mask.restype = c_int
+    lib.steel_topk_block_mask.argtypes = [c_void_p, c_void_p] + [c_int] * 10 + [c_void_p, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

@@ -1,0 +1,175 @@
+// Block-mask producer on gfx950: for every query block, the key blocks whose
+// mean-pooled keys score highest against the mean-pooled queries (top-k of
+// the causal candidates, ties to the smaller block), plus the diagonal block.
+//
+// The paper builds its masks on the compute core instead of fetching them
+// (Section III-B) and runs any block mask through the three tile classes of
+// Section IV-A; this is the selection rule the sparse workload is defined
+// with, moved onto the GPU ahead of the index build.
+//
+// Floating point decides which blocks are kept, so the arithmetic is fixed:
+// float64 throughout, each block sum adds its rows in increasing order, the
+// mean divides that sum by the row count (correctly rounded), and each score
+// adds the D products in increasing d with every product and sum rounded on
+// its own (no fused multiply-add).  Three launches:
+//   block_means   one workgroup per (head, block) of Q and of K, one thread
+//                 per column
+//   block_scores  64 x 64 score tiles per workgroup from LDS-staged means
+//                 (tiles above the diagonal skipped when causal)
+//   topk_select   one workgroup per (head, query block): bitonic sort of the
+//                 candidates in LDS, then the mask row
+#include <climits>
+
+#include "internal.h"
+
+namespace steel {
+
+constexpr int kMaxSelect = 4096;  // key blocks one select workgroup can rank
+
+__global__ __launch_bounds__(128) void k_block_means(const __bf16* __restrict__ x, int S, int nb,
+                                                     int D, double* __restrict__ out) {
+  const int g = blockIdx.x;  // (head, block)
+  const int d = threadIdx.x;
+  if (d >= D) return;
+  const int bh = g / nb, bi = g - bh * nb;
+  const int r0 = bi * kBlk;
+  const int cnt = min(kBlk, S - r0);
+  const __bf16* p = x + ((size_t)bh * S + r0) * D + d;
+  double acc = 0.0;
+  for (int r = 0; r < cnt; ++r) acc = acc + (double)(float)p[(size_t)r * D];
+  out[(size_t)g * D + d] = acc / (double)cnt;
+}
+
+// scores[bh][qb][kb] = dot(qm[bh][qb], km[bh / G][kb]) for one 64 x 64 tile.
+// Thread t owns rows 4*(t/16) .. +3 and columns 4*(t%16) .. +3 of the tile.
+__global__ __launch_bounds__(256) void k_block_scores(const double* __restrict__ qm,
+                                                      const double* __restrict__ km, int nQB,
+                                                      int nKB, int D, int G, int Hq, int Hkv,
+                                                      int causal, int ntq, int ntk,
+                                                      double* __restrict__ scores) {
+#pragma clang fp contract(off)
+  constexpr int DC = 32;  // d chunk staged in LDS
+  __shared__ double qs[DC][kBlk + 1];  // + 1: the staging writes step over banks
+  __shared__ double ks[DC][kBlk + 1];
+  const int t = threadIdx.x;
+  int g = blockIdx.x;
+  const int tk = g % ntk;
+  g /= ntk;
+  const int tq = g % ntq;
+  const int bh = g / ntq;  // b * Hq + h
+  if (causal && tk > tq) return;  // every kb of the tile lies past every qb
+  const int b = bh / Hq, h = bh - b * Hq;
+  const double* qrow = qm + (size_t)bh * nQB * D;
+  const double* krow = km + ((size_t)b * Hkv + h / G) * nKB * D;
+  const int i0 = 4 * (t >> 4), j0 = 4 * (t & 15);
+  double acc[4][4];
+#pragma unroll
+  for (int a = 0; a < 4; ++a)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[a][c] = 0.0;
+  for (int d0 = 0; d0 < D; d0 += DC) {
+    // stage qm / km rows of the tile, d-major
+    for (int e = t; e < kBlk * DC; e += 256) {
+      const int r = e / DC, dd = e - r * DC;
+      const int qb = tq * kBlk + r, kb = tk * kBlk + r;
+      qs[dd][r] = qb < nQB ? qrow[(size_t)qb * D + d0 + dd] : 0.0;
+      ks[dd][r] = kb < nKB ? krow[(size_t)kb * D + d0 + dd] : 0.0;
+    }
+    __syncthreads();
+    for (int dd = 0; dd < DC; ++dd) {
+      double a[4], c[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] = qs[dd][i0 + u];
+        c[u] = ks[dd][j0 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) acc[u][w] = acc[u][w] + a[u] * c[w];
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int qb = tq * kBlk + i0 + u;
+    if (qb >= nQB) continue;
+    double* out = scores + ((size_t)bh * nQB + qb) * nKB;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int kb = tk * kBlk + j0 + w;
+      if (kb < nKB) out[kb] = acc[u][w];
+    }
+  }
+}
+
+// Does candidate a come before candidate b (larger score, then smaller kb)?
+__device__ __forceinline__ bool before(double sa, int ia, double sb, int ib) {
+  return sa > sb || (sa == sb && ia < ib);
+}
+
+__global__ __launch_bounds__(256) void k_topk_select(const double* __restrict__ scores, int nQB,
+                                                     int nKB, int causal, long long keep_num,
+                                                     long long keep_den,
+                                                     uint8_t* __restrict__ mask) {
+  __shared__ double s[kMaxSelect];
+  __shared__ int id[kMaxSelect];
+  __shared__ uint8_t flag[kMaxSelect];
+  const int t = threadIdx.x;
+  const size_t row = blockIdx.x;  // (b * Hq + h) * nQB + qb
+  const int qb = (int)(row % (size_t)nQB);
+  const int ncand = causal ? min(qb + 1, nKB) : nKB;
+  const int keep = (int)((keep_num * ncand + keep_den - 1) / keep_den);
+  int n2 = 1;
+  while (n2 < ncand) n2 <<= 1;
+  const double* src = scores + row * nKB;
+  for (int j = t; j < n2; j += 256) {
+    s[j] = j < ncand ? src[j] : -INFINITY;
+    id[j] = j;
+  }
+  for (int j = t; j < nKB; j += 256) flag[j] = 0;
+  __syncthreads();
+  // bitonic sort of n2 entries into "before" order
+  for (int k = 2; k <= n2; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = t; i < n2; i += 256) {
+        const int l = i ^ j;
+        if (l > i) {
+          const bool up = (i & k) == 0;
+          const double si = s[i], sl = s[l];
+          const int ii = id[i], il = id[l];
+          const bool swap = up ? before(sl, il, si, ii) : before(si, ii, sl, il);
+          if (swap) {
+            s[i] = sl;
+            s[l] = si;
+            id[i] = il;
+            id[l] = ii;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int j = t; j < keep; j += 256) flag[id[j]] = 1;
+  if (t == 0 && qb < nKB) flag[qb] = 1;
+  __syncthreads();
+  uint8_t* dst = mask + row * nKB;
+  for (int kb = t; kb < nKB; kb += 256) dst[kb] = flag[kb];
+}
+
+hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, int keep_num,
+                            int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
+                            hipStream_t s) {
+  const int ntq = (p.nQB + kBlk - 1) / kBlk, ntk = (p.nKB + kBlk - 1) / kBlk;
+  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hq * p.nQB), dim3(p.D), 0, s, q, p.S_q, p.nQB,
+                     p.D, qm);
+  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hkv * p.nKB), dim3(p.D), 0, s, k, p.S_k, p.nKB,
+                     p.D, km);
+  hipLaunchKernelGGL(k_block_scores, dim3(p.B * p.Hq * ntq * ntk), dim3(256), 0, s, qm, km, p.nQB,
+                     p.nKB, p.D, p.G, p.Hq, p.Hkv, p.causal, ntq, ntk, scores);
+  hipLaunchKernelGGL(k_topk_select, dim3(p.B * p.Hq * p.nQB), dim3(256), 0, s, scores, p.nQB,
+                     p.nKB, p.causal, (long long)keep_num, (long long)keep_den, mask);
+  return hipGetLastError();
+}
+
+}  // namespace steel

@@ -72,6 +72,13 @@ constexpr int kFastRows = 12288;
 hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const IndexBuffers& w,
                               hipStream_t stream);
 
+// Enqueue the top-k mean-pooled block selection (block_select.hip): writes the
+// whole block mask [B][Hq][nQB][nKB].  qm, km, scores: float64 workspace of
+// B*Hq*nQB*D, B*Hkv*nKB*D and B*Hq*nQB*nKB values.  Needs nKB <= 4096.
+hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, int keep_num,
+                            int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
+                            hipStream_t stream);
+
 // Enqueue the fused attention over both item lists.
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
                             float* out, float scale, const IndexBuffers& w, hipStream_t stream);

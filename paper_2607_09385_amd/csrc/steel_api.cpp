@@ -309,6 +309,47 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out, int B
   return STEEL_OK;
 }
 
+int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, int S_q, int S_k,
+                          int D, int blk, int causal, int keep_num, int keep_den,
+                          uint8_t* block_mask, void* stream) {
+  g_err.clear();
+  if (!q || !k || !block_mask)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q, k and block_mask must be non-NULL device pointers");
+  if (!aligned16(q) || !aligned16(k))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "q and k must be 16-byte aligned");
+  if (keep_num < 1 || keep_den < 1 || keep_num > keep_den)
+    return fail(STEEL_ERR_INVALID_ARGUMENT,
+                "keep fraction %d/%d must satisfy 1 <= keep_num <= keep_den", keep_num, keep_den);
+  steel::Problem p{};
+  int rc = check_shape(B, Hq, Hkv, S_q, S_k, blk, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  if (D != 64 && D != 128) return fail(STEEL_ERR_UNSUPPORTED, "D=%d not supported (64 or 128)", D);
+  p.D = D;
+  if (p.nKB > 4096)
+    return fail(STEEL_ERR_UNSUPPORTED, "%d key blocks: the selection ranks at most 4096", p.nKB);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
+  hipMemPool_t pool;
+  hipError_t e = device_pool(dev, &pool);
+  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
+  const size_t n_qm = (size_t)B * Hq * p.nQB * D, n_km = (size_t)B * Hkv * p.nKB * D;
+  const size_t n_sc = (size_t)B * Hq * p.nQB * p.nKB;
+  const size_t o_km = align256(n_qm * sizeof(double)), o_sc = o_km + align256(n_km * sizeof(double));
+  const size_t total = o_sc + align256(n_sc * sizeof(double));
+  char* ws = nullptr;
+  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), total, pool, s);
+  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
+  e = steel::launch_topk_mask(p, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
+                              keep_num, keep_den, block_mask, reinterpret_cast<double*>(ws),
+                              reinterpret_cast<double*>(ws + o_km), reinterpret_cast<double*>(ws + o_sc),
+                              s);
+  hipError_t ef = hipFreeAsync(ws, s);
+  if (e != hipSuccess) return hip_fail(e, "launching kernels");
+  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
+  return STEEL_OK;
+}
+
 int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k, int blk,
                       int causal, int32_t* row_ptr, uint32_t* col, int32_t* order, void* stream) {
   g_err.clear();

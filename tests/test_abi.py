@@ -146,3 +146,20 @@ def test_window_forms_reject_invalid_window():
     st = lib.steel_attn_fwd_window(FAKE, FAKE, FAKE, FAKE, 1, 4, 2, 128, 128, 96, 64, 0.125, 1,
                                    2, 0, None)
     assert st == 2 and "D=96" in _lib.last_error()
+
+
+def test_topk_block_mask_rejects_invalid():
+    lib = _lib.load()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 1, 1, 10, None, None)
+    assert st == 1 and "non-NULL" in _lib.last_error()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 1, 0, 10, FAKE, None)
+    assert st == 1 and "keep fraction" in _lib.last_error()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 1, 11, 10, FAKE, None)
+    assert st == 1 and "keep fraction" in _lib.last_error()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 4, 2, 128, 128, 80, 64, 1, 1, 10, FAKE, None)
+    assert st == 2 and "D=80" in _lib.last_error()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 4, 2, 128, 64 * 4097, 64, 64, 1, 1, 10, FAKE,
+                                   None)
+    assert st == 2 and "4096" in _lib.last_error()
+    st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 3, 2, 128, 128, 64, 64, 1, 1, 10, FAKE, None)
+    assert st == 1 and "multiple" in _lib.last_error()
