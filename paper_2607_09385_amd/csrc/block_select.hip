@@ -12,31 +12,40 @@
 // mean divides that sum by the row count (correctly rounded), and each score
 // adds the D products in increasing d with every product and sum rounded on
 // its own (no fused multiply-add).  Three launches:
-//   block_means   one workgroup per (head, block) of Q and of K, one thread
-//                 per column
+//   block_means   one workgroup per (head, block) of Q and of K: the rows
+//                 staged in LDS, one thread per column
 //   block_scores  64 x 64 score tiles per workgroup from LDS-staged means
 //                 (tiles above the diagonal skipped when causal)
-//   topk_select   one workgroup per (head, query block): bitonic sort of the
+//   topk_select   one wave per (head, query block): bitonic sort of the
 //                 candidates in LDS, then the mask row
+#include <algorithm>
 #include <climits>
 
 #include "internal.h"
 
 namespace steel {
 
-constexpr int kMaxSelect = 4096;  // key blocks one select workgroup can rank
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 
+// One workgroup per (head, block): the block's rows (contiguous in memory)
+// are staged into LDS with 16-byte loads, then thread d sums column d over the
+// rows in increasing order.
 __global__ __launch_bounds__(128) void k_block_means(const __bf16* __restrict__ x, int S, int nb,
                                                      int D, double* __restrict__ out) {
+  __shared__ __attribute__((aligned(16))) __bf16 tile[kBlk * 128];
   const int g = blockIdx.x;  // (head, block)
-  const int d = threadIdx.x;
-  if (d >= D) return;
   const int bh = g / nb, bi = g - bh * nb;
   const int r0 = bi * kBlk;
   const int cnt = min(kBlk, S - r0);
-  const __bf16* p = x + ((size_t)bh * S + r0) * D + d;
+  const __bf16* p = x + ((size_t)bh * S + r0) * D;
+  const int nvec = cnt * D / 8;
+  for (int v = threadIdx.x; v < nvec; v += 128)
+    *(bf16x8_t*)(tile + 8 * v) = *(const bf16x8_t*)(p + 8 * v);
+  __syncthreads();
+  const int d = threadIdx.x;
+  if (d >= D) return;
   double acc = 0.0;
-  for (int r = 0; r < cnt; ++r) acc = acc + (double)(float)p[(size_t)r * D];
+  for (int r = 0; r < cnt; ++r) acc = acc + (double)(float)tile[r * D + d];
   out[(size_t)g * D + d] = acc / (double)cnt;
 }
 
@@ -49,8 +58,10 @@ __global__ __launch_bounds__(256) void k_block_scores(const double* __restrict__
                                                       double* __restrict__ scores) {
 #pragma clang fp contract(off)
   constexpr int DC = 32;  // d chunk staged in LDS
-  __shared__ double qs[DC][kBlk + 1];  // + 1: the staging writes step over banks
-  __shared__ double ks[DC][kBlk + 1];
+  // rows padded by 2 doubles: the staging writes step over banks and every row
+  // stays 16-byte aligned for the paired operand reads
+  __shared__ __attribute__((aligned(16))) double qs[DC][kBlk + 2];
+  __shared__ __attribute__((aligned(16))) double ks[DC][kBlk + 2];
   const int t = threadIdx.x;
   int g = blockIdx.x;
   const int tk = g % ntk;
@@ -76,17 +87,27 @@ __global__ __launch_bounds__(256) void k_block_scores(const double* __restrict__
       ks[dd][r] = kb < nKB ? krow[(size_t)kb * D + d0 + dd] : 0.0;
     }
     __syncthreads();
-    for (int dd = 0; dd < DC; ++dd) {
-      double a[4], c[4];
+    // operands of step dd + 1 are read while step dd computes
+    double a[2][4], c[2][4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        a[u] = qs[dd][i0 + u];
-        c[u] = ks[dd][j0 + u];
+    for (int u = 0; u < 4; ++u) {
+      a[0][u] = qs[0][i0 + u];
+      c[0][u] = ks[0][j0 + u];
+    }
+#pragma unroll
+    for (int dd = 0; dd < DC; ++dd) {
+      const int cur = dd & 1;
+      if (dd + 1 < DC) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          a[cur ^ 1][u] = qs[dd + 1][i0 + u];
+          c[cur ^ 1][u] = ks[dd + 1][j0 + u];
+        }
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u)
 #pragma unroll
-        for (int w = 0; w < 4; ++w) acc[u][w] = acc[u][w] + a[u] * c[w];
+        for (int w = 0; w < 4; ++w) acc[u][w] = acc[u][w] + a[cur][u] * c[cur][w];
     }
     __syncthreads();
   }
@@ -108,67 +129,85 @@ __device__ __forceinline__ bool before(double sa, int ia, double sb, int ib) {
   return sa > sb || (sa == sb && ia < ib);
 }
 
+// One wave per (head, query block) row, blockDim/64 rows per workgroup.  Each wave
+// has its own LDS segment (n2max scores, n2max indices, nKB flags); the
+// steps of the sort are separated by a wave-level wait, not a barrier.
+__device__ __forceinline__ void wave_lds_sync() {
+  // this wave's LDS accesses are done, and the compiler moves none across
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
 __global__ __launch_bounds__(256) void k_topk_select(const double* __restrict__ scores, int nQB,
-                                                     int nKB, int causal, long long keep_num,
-                                                     long long keep_den,
+                                                     int nKB, int n2max, size_t seg, int causal,
+                                                     long long keep_num, long long keep_den,
+                                                     long long n_rows,
                                                      uint8_t* __restrict__ mask) {
-  __shared__ double s[kMaxSelect];
-  __shared__ int id[kMaxSelect];
-  __shared__ uint8_t flag[kMaxSelect];
-  const int t = threadIdx.x;
-  const size_t row = blockIdx.x;  // (b * Hq + h) * nQB + qb
-  const int qb = (int)(row % (size_t)nQB);
+  extern __shared__ __attribute__((aligned(16))) char sel_lds[];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * (blockDim.x >> 6) + w;  // (b*Hq + h)*nQB + qb
+  if (row >= n_rows) return;  // the whole wave; no workgroup barrier follows
+  char* base = sel_lds + (size_t)w * seg;
+  double* s = reinterpret_cast<double*>(base);
+  int* id = reinterpret_cast<int*>(base + 8 * (size_t)n2max);
+  uint8_t* flag = reinterpret_cast<uint8_t*>(base + 12 * (size_t)n2max);
+  const int qb = (int)(row % nQB);
   const int ncand = causal ? min(qb + 1, nKB) : nKB;
   const int keep = (int)((keep_num * ncand + keep_den - 1) / keep_den);
   int n2 = 1;
   while (n2 < ncand) n2 <<= 1;
-  const double* src = scores + row * nKB;
-  for (int j = t; j < n2; j += 256) {
+  const double* src = scores + (size_t)row * nKB;
+  for (int j = lane; j < n2; j += 64) {
     s[j] = j < ncand ? src[j] : -INFINITY;
     id[j] = j;
   }
-  for (int j = t; j < nKB; j += 256) flag[j] = 0;
-  __syncthreads();
-  // bitonic sort of n2 entries into "before" order
+  for (int j = lane; j < nKB; j += 64) flag[j] = 0;
+  wave_lds_sync();
+  // bitonic sort of n2 entries into "before" order; in each step every lane
+  // takes whole compare-exchange pairs (i, i + j), i with bit j clear
   for (int k = 2; k <= n2; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = t; i < n2; i += 256) {
-        const int l = i ^ j;
-        if (l > i) {
-          const bool up = (i & k) == 0;
-          const double si = s[i], sl = s[l];
-          const int ii = id[i], il = id[l];
-          const bool swap = up ? before(sl, il, si, ii) : before(si, ii, sl, il);
-          if (swap) {
-            s[i] = sl;
-            s[l] = si;
-            id[i] = il;
-            id[l] = ii;
-          }
+      for (int pr = lane; pr < (n2 >> 1); pr += 64) {
+        const int i = ((pr & ~(j - 1)) << 1) | (pr & (j - 1));
+        const int l = i + j;
+        const bool up = (i & k) == 0;
+        const double si = s[i], sl = s[l];
+        const int ii = id[i], il = id[l];
+        const bool swap = up ? before(sl, il, si, ii) : before(si, ii, sl, il);
+        if (swap) {
+          s[i] = sl;
+          s[l] = si;
+          id[i] = il;
+          id[l] = ii;
         }
       }
-      __syncthreads();
+      wave_lds_sync();
     }
   }
-  for (int j = t; j < keep; j += 256) flag[id[j]] = 1;
-  if (t == 0 && qb < nKB) flag[qb] = 1;
-  __syncthreads();
-  uint8_t* dst = mask + row * nKB;
-  for (int kb = t; kb < nKB; kb += 256) dst[kb] = flag[kb];
+  for (int j = lane; j < keep; j += 64) flag[id[j]] = 1;
+  if (lane == 0 && qb < nKB) flag[qb] = 1;
+  wave_lds_sync();
+  uint8_t* dst = mask + (size_t)row * nKB;
+  for (int kb = lane; kb < nKB; kb += 64) dst[kb] = flag[kb];
 }
 
 hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, int keep_num,
                             int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
                             hipStream_t s) {
   const int ntq = (p.nQB + kBlk - 1) / kBlk, ntk = (p.nKB + kBlk - 1) / kBlk;
-  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hq * p.nQB), dim3(p.D), 0, s, q, p.S_q, p.nQB,
+  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hq * p.nQB), dim3(128), 0, s, q, p.S_q, p.nQB,
                      p.D, qm);
-  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hkv * p.nKB), dim3(p.D), 0, s, k, p.S_k, p.nKB,
+  hipLaunchKernelGGL(k_block_means, dim3(p.B * p.Hkv * p.nKB), dim3(128), 0, s, k, p.S_k, p.nKB,
                      p.D, km);
   hipLaunchKernelGGL(k_block_scores, dim3(p.B * p.Hq * ntq * ntk), dim3(256), 0, s, qm, km, p.nQB,
                      p.nKB, p.D, p.G, p.Hq, p.Hkv, p.causal, ntq, ntk, scores);
-  hipLaunchKernelGGL(k_topk_select, dim3(p.B * p.Hq * p.nQB), dim3(256), 0, s, scores, p.nQB,
-                     p.nKB, p.causal, (long long)keep_num, (long long)keep_den, mask);
+  int n2max = 1;
+  while (n2max < p.nKB) n2max <<= 1;
+  const size_t seg = (12 * (size_t)n2max + (size_t)p.nKB + 15) & ~(size_t)15;  // per wave
+  const int wpg = (int)std::max<size_t>(1, std::min<size_t>(4, 65536 / seg));   // waves per group
+  const long long rows = (long long)p.B * p.Hq * p.nQB;
+  hipLaunchKernelGGL(k_topk_select, dim3((unsigned)((rows + wpg - 1) / wpg)), dim3(64 * wpg),
+                     wpg * seg, s, scores, p.nQB, p.nKB, n2max, seg, p.causal, (long long)keep_num,
+                     (long long)keep_den, rows, mask);
   return hipGetLastError();
 }
 

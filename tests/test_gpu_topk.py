@@ -35,6 +35,8 @@ CASES = [
     ("keep_all", 1, 1, 1, 640, 640, 128, True, 1, 1),
     ("many_key_blocks", 1, 2, 1, 300, 64 * 300 + 17, 64, False, 1, 20),
     ("one_block", 1, 1, 1, 10, 10, 64, True, 1, 10),
+    # 2000 key blocks: two rows per select workgroup instead of four
+    ("wide_rows", 1, 2, 1, 200, 64 * 2000 - 5, 64, False, 1, 10),
 ]
 
 
