@@ -338,6 +338,142 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
     return line
 
 
+def unfused_attention(qd, kd, vd, hidden, scale):
+    """Layer-by-layer attention on the same GPU (the comparison of Section V-C:
+    every stage writes its result to HBM and the next reads it back):
+    S = scale * Q K^T (hipBLASLt bf16 GEMM, materialised), masked with -inf,
+    P = softmax(S) (materialised, bf16), O = P V (hipBLASLt).  ``hidden`` is the
+    element mask of the scores that are not visible (bool [B, Hq, S_q, S_k])."""
+    import torch
+    B, Hq, S_q, D = qd.shape
+    Hkv, S_k = kd.shape[1], kd.shape[2]
+    G = Hq // Hkv
+    q3 = qd.reshape(B * Hkv, G * S_q, D)
+    kt = kd.reshape(B * Hkv, S_k, D).transpose(1, 2).contiguous()
+    a = torch.empty((B * Hkv, G * S_q, S_k), dtype=torch.bfloat16, device=qd.device)
+    torch.baddbmm(a, q3, kt, beta=0.0, alpha=scale, out=a)
+    a = a.view(B, Hq, S_q, S_k).masked_fill_(hidden, float("-inf"))
+    p = torch.softmax(a, dim=-1)
+    o = torch.bmm(p.view(B * Hkv, G * S_q, S_k), vd.reshape(B * Hkv, S_k, D))
+    return o.view(B, Hq, S_q, D)
+
+
+def hidden_scores(md, B, Hq, S_q, S_k, causal, dev):
+    """bool [B, Hq, S_q, S_k]: True where the block mask or the causal
+    structure hides the score."""
+    import torch
+    if md is None:
+        vis = torch.ones((B, Hq, S_q, S_k), dtype=torch.bool, device=dev)
+    else:
+        vis = md.bool().repeat_interleave(64, 2).repeat_interleave(64, 3)[:, :, :S_q, :S_k]
+    if causal:
+        vis = vis & torch.ones((S_q, S_k), dtype=torch.bool, device=dev).tril(diagonal=S_k - S_q)
+    return (~vis).contiguous()
+
+
+def bench_unfused(name, steps, warmup):
+    """One JSON line: the layer-by-layer baseline against the fused call on
+    the same workload and GPU, with the HBM bytes each moves by construction."""
+    import torch
+    import workloads
+    import paper_2607_09385_amd as steel
+
+    steel.load()
+    cfg = workloads.CONFIGS[name]
+    q, k, v, mask = workloads.make_workload(cfg)
+    dev = torch.device("cuda:0")
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    md = None if mask is None else torch.from_numpy(mask).to(dev)
+    hidden = hidden_scores(md, cfg.B, cfg.Hq, cfg.S_q, cfg.S_k, cfg.causal, dev)
+    counts = live_tile_counts(mask, cfg.B, cfg.Hq, cfg.S_q, cfg.S_k, cfg.causal)
+    f_live = 4.0 * 64 * 64 * cfg.D * int(counts.sum())
+    out = torch.empty((cfg.B, cfg.Hq, cfg.S_q, cfg.D), dtype=torch.float32, device=dev)
+
+    def timed(fn, n_warm, n):
+        for _ in range(n_warm):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(n):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / n
+
+    t_unf = timed(lambda: unfused_attention(qd, kd, vd, hidden, cfg.scale), warmup, steps)
+    t_fus = timed(lambda: steel.attn_fwd(qd, kd, vd, md, scale=cfg.scale, causal=cfg.causal, out=out),
+                  warmup, steps)
+    o_unf = unfused_attention(qd, kd, vd, hidden, cfg.scale).float()
+    steel.attn_fwd(qd, kd, vd, md, scale=cfg.scale, causal=cfg.causal, out=out)
+    torch.cuda.synchronize()
+    diff = (o_unf - out).abs()
+    n_sc = cfg.B * cfg.Hq * cfg.S_q * cfg.S_k
+    qkv = 2 * (q.numel() + k.numel() + v.numel())
+    # by construction: GEMM writes S (2 B/score); the mask pass reads S and the
+    # mask and writes S (5 B); softmax reads S, writes P (4 B); the PV GEMM
+    # reads P (2 B); plus Q, K, V read and O written (bf16)
+    unf_bytes = qkv + 13 * n_sc + 2 * q.numel()
+    fus_bytes = qkv + 4 * q.numel() + (0 if mask is None else mask.size)
+    return {
+        "baseline": "layer-by-layer attention (hipBLASLt GEMMs, softmax and mask passes, scores and P materialised in bf16)",
+        "workload": name,
+        "unfused_ms": round(t_unf * 1e3, 3),
+        "fused_ms": round(t_fus * 1e3, 3),
+        "speedup_fused": round(t_unf / t_fus, 2),
+        "unfused_effective_tflops": round(f_live / t_unf / 1e12, 2),
+        "fused_effective_tflops": round(f_live / t_fus / 1e12, 2),
+        "hbm_bytes_model": {"unfused": unf_bytes, "fused_algorithmic": fus_bytes},
+        "max_abs_diff_vs_fused": float(diff.max().item()),
+        "mean_abs_diff_vs_fused": float(diff.mean().item()),
+        "steps": steps, "warmup": warmup,
+    }
+
+
+def unfused_traffic_run(name):
+    """Workload for counter passes over the layer-by-layer baseline: one warm
+    call, then a float32 elementwise add of COPY_BYTES, one unfused call, and
+    the add again (the two adds bracket the call's dispatches and scale the
+    counters)."""
+    import torch
+    import workloads
+
+    cfg = workloads.CONFIGS[name]
+    q, k, v, mask = workloads.make_workload(cfg)
+    dev = torch.device("cuda:0")
+    qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
+    md = None if mask is None else torch.from_numpy(mask).to(dev)
+    hidden = hidden_scores(md, cfg.B, cfg.Hq, cfg.S_q, cfg.S_k, cfg.causal, dev)
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    unfused_attention(qd, kd, vd, hidden, cfg.scale)
+    torch.cuda.synchronize()
+    torch.add(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    unfused_attention(qd, kd, vd, hidden, cfg.scale)
+    torch.cuda.synchronize()
+    torch.add(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(f"[unfused-traffic-run] {name}: one unfused call between two {COPY_BYTES} B adds", flush=True)
+
+
+def unfused_traffic_from(fetch_dir, write_dir):
+    """HBM bytes of the unfused call from the two counter passes over
+    ``--unfused-traffic-run``: the dispatches between the last two adds."""
+    import csv
+    out = {}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = [r for r in csv.DictReader(open(os.path.join(d, "run_counter_collection.csv")))
+                if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        adds = [i for i, r in enumerate(rows) if "elementwise" in r["Kernel_Name"] and "add" in r["Kernel_Name"]]
+        a, b = adds[-2], adds[-1]
+        scale = COPY_BYTES / (float(rows[a]["Counter_Value"]) * 1024.0)
+        between = rows[a + 1:b]
+        out[counter] = {"bytes": sum(float(r["Counter_Value"]) for r in between) * 1024.0 * scale,
+                        "dispatches": len(between), "scale": scale}
+    out["total_bytes"] = out["FETCH_SIZE"]["bytes"] + out["WRITE_SIZE"]["bytes"]
+    print(json.dumps(out, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -351,7 +487,16 @@ def main():
                     help="workload for the rocprofv3 FETCH_SIZE / WRITE_SIZE passes")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="record HBM bytes per run from the two counter passes")
+    ap.add_argument("--unfused", action="store_true",
+                    help="layer-by-layer baseline against the fused call (one JSON line)")
+    ap.add_argument("--unfused-traffic-run", action="store_true",
+                    help="workload for counter passes over the layer-by-layer baseline")
+    ap.add_argument("--unfused-traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="HBM bytes of one layer-by-layer call from the two counter passes")
     args = ap.parse_args()
+    if args.unfused_traffic_from:
+        unfused_traffic_from(*args.unfused_traffic_from)
+        return
     if args.traffic_from:
         traffic_from(args.traffic_from[0], args.traffic_from[1], args.workload)
         return
@@ -363,6 +508,13 @@ def main():
         sys.exit(2)
     if args.traffic_run:
         traffic_run(args.workload, args.steps if args.steps != 50 else 5)
+        return
+    if args.unfused_traffic_run:
+        unfused_traffic_run(args.workload)
+        return
+    if args.unfused:
+        print(json.dumps(bench_unfused(args.workload, args.steps if args.steps != 50 else 10,
+                                       args.warmup if args.warmup != 25 else 3)), flush=True)
         return
     import workloads
     names = workloads.CONFIG_ORDER if args.all else [args.workload]
