@@ -14,7 +14,9 @@ It is written from the paper's definitions, independently of the GPU code:
   per-query-block list, plus the heaviest-first work order that stands in for
   the sparsity-aware placement of Section IV-C;
 * ``block_select`` -- the mask producer that runs before the pass: top-k key
-  blocks per query block by mean-pooled query/key score, plus the diagonal.
+  blocks per query block by mean-pooled query/key score, plus the diagonal;
+* ``lse_merge``   -- the per-row log-sum-exp of the scores and the rule that
+  merges partial results computed over disjoint key chunks.
 
 Every function is pinned by tests against things other than itself: brute
 force on tiny inputs, closed forms, invariants and an independent library
@@ -23,3 +25,4 @@ routine (see the module docstrings).
 from .masked_attention import attention, attention_rows, element_visibility, kv_head  # noqa: F401
 from .block_index import N_BINS, build_index, count_bin, tile_classes, work_order  # noqa: F401
 from .block_select import block_means, block_scores, keep_count, topk_meanpool_mask  # noqa: F401
+from .lse_merge import attention_lse, merge_partials  # noqa: F401

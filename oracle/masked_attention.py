@@ -43,10 +43,11 @@ def kv_head(h: int, Hq: int, Hkv: int) -> int:
 
 
 def element_visibility(block_row_bits: np.ndarray, rows: np.ndarray, S_q: int,
-                       S_k: int, blk: int, causal: bool) -> np.ndarray:
+                       S_k: int, blk: int, causal: bool, offset=None) -> np.ndarray:
     """Boolean [len(rows), S_k]: which keys each listed query row may see.
 
     ``block_row_bits`` is the [nQB, nKB] block mask of one (b, h), or None.
+    ``offset``: causal key limit ``j <= i + offset`` (default S_k - S_q).
     """
     rows = np.asarray(rows, dtype=np.int64)
     cols = np.arange(S_k, dtype=np.int64)
@@ -56,7 +57,7 @@ def element_visibility(block_row_bits: np.ndarray, rows: np.ndarray, S_q: int,
         bits = np.asarray(block_row_bits) != 0
         vis = bits[rows // blk][:, cols // blk]
     if causal:
-        vis &= cols[None, :] <= rows[:, None] + (S_k - S_q)
+        vis &= cols[None, :] <= rows[:, None] + ((S_k - S_q) if offset is None else offset)
     return vis
 
 
