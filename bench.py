@@ -474,6 +474,40 @@ def unfused_traffic_from(fetch_dir, write_dir):
     print(json.dumps(out, indent=1))
 
 
+def bench_merge(name, parts, steps, warmup):
+    """Time of steel_attn_merge over ``parts`` partial outputs of the
+    workload's output shape, against the HBM roofline (each part's O and lse
+    read once, O and lse written once)."""
+    import torch
+    import workloads
+    import paper_2607_09385_amd as steel
+
+    steel.load()
+    cfg = workloads.CONFIGS[name]
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(0)
+    o = torch.randn((parts, cfg.B, cfg.Hq, cfg.S_q, cfg.D), generator=g, device=dev)
+    l = torch.randn((parts, cfg.B, cfg.Hq, cfg.S_q), generator=g, device=dev)
+    out = torch.empty(o.shape[1:], device=dev)
+    lo = torch.empty(l.shape[1:], device=dev)
+    for _ in range(warmup):
+        steel.attn_merge(o, l, out=out, lse_out=lo)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        steel.attn_merge(o, l, out=out, lse_out=lo)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) / 1e3 / steps
+    nbytes = 4 * (o.numel() + l.numel() + out.numel() + lo.numel())
+    return {"call": "steel_attn_merge", "workload_shape": name, "parts": parts,
+            "us": round(t * 1e6, 2),
+            "roofline": {"bound": "hbm", "achieved": round(nbytes / t / 1e9, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(nbytes / t / 1e9 / HBM_PEAK_GBS, 4),
+                         "algorithmic_bytes": nbytes}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -489,6 +523,8 @@ def main():
                     help="record HBM bytes per run from the two counter passes")
     ap.add_argument("--unfused", action="store_true",
                     help="layer-by-layer baseline against the fused call (one JSON line)")
+    ap.add_argument("--merge", type=int, default=0, metavar="PARTS",
+                    help="time steel_attn_merge over PARTS partial outputs of the workload's shape")
     ap.add_argument("--unfused-traffic-run", action="store_true",
                     help="workload for counter passes over the layer-by-layer baseline")
     ap.add_argument("--unfused-traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -508,6 +544,9 @@ def main():
         sys.exit(2)
     if args.traffic_run:
         traffic_run(args.workload, args.steps if args.steps != 50 else 5)
+        return
+    if args.merge:
+        print(json.dumps(bench_merge(args.workload, args.merge, args.steps, args.warmup)), flush=True)
         return
     if args.unfused_traffic_run:
         unfused_traffic_run(args.workload)

@@ -133,6 +133,49 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out,
                    void* stream);
 
 /*
+ * steel_attn_fwd with two additions for work split over key chunks
+ * (chunked prefill, keys held on several devices):
+ *
+ *   lse            float [B][Hq][S_q] device buffer, or NULL: receives each
+ *                  query row's log sum_j exp(scale * q_i . k_j) over its
+ *                  visible keys (natural log; -inf when no key is visible).
+ *                  It is the row statistic Algorithm 1 carries (running
+ *                  maximum m and sum l: lse = m + log l).
+ *   causal_offset  when causal, key j is visible to query i iff
+ *                  j <= i + causal_offset (steel_attn_fwd uses S_k - S_q);
+ *                  a chunk [k0, k1) of a sequence of S_k_total keys is passed
+ *                  as its own K, V with causal_offset = S_k_total - S_q - k0.
+ *                  Ignored when causal == 0; otherwise within [-2^30, 2^30].
+ *
+ * Everything else as steel_attn_fwd; with lse == NULL and causal_offset =
+ * S_k - S_q the output is bitwise that of steel_attn_fwd.
+ */
+int steel_attn_fwd_ex(const void* q, const void* k, const void* v,
+                      const uint8_t* block_mask, void* out, float* lse,
+                      int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                      float scale, int causal, int causal_offset, void* stream);
+
+/*
+ * Merge of partial results over disjoint key sets: with n_parts outputs O_c
+ * and row log-sum-exps lse_c (from steel_attn_fwd_ex over each key chunk),
+ *   out = sum_c exp(lse_c - L) O_c / sum_c exp(lse_c - L),   L = max_c lse_c
+ *   lse_out = L + log sum_c exp(lse_c - L)
+ * per row; rows with every lse_c = -inf get out = 0 and lse_out = -inf.
+ *
+ *   o_parts    float [n_parts][rows][D] device, 16-byte aligned
+ *   lse_parts  float [n_parts][rows] device
+ *   rows       rows per part (B*Hq*S_q for attention outputs), >= 1
+ *   D          positive multiple of 4
+ *   out        float [rows][D] device, 16-byte aligned (may not alias a part)
+ *   lse_out    float [rows] device, or NULL
+ *
+ * Invalid arguments: STEEL_ERR_INVALID_ARGUMENT before any HIP call.  The
+ * call only enqueues; it allocates nothing.
+ */
+int steel_attn_merge(const float* o_parts, const float* lse_parts, int n_parts, long long rows,
+                     int D, float* out, float* lse_out, void* stream);
+
+/*
  * Structured-mask forms: the block mask is generated from block coordinates
  * instead of read from a tensor (the paper builds masks on the core rather
  * than fetching them, Section III-B, and names windowed attention among the

@@ -87,6 +87,71 @@ def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal:
     return out
 
 
+def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal: bool = True,
+                 causal_offset: Optional[int] = None, blk: int = BLK, out=None, lse=None,
+                 stream=None):
+    """``attn_fwd`` that also returns the row log-sum-exp (fp32 [B, Hq, S_q],
+    natural log, -inf for rows with no visible key) and takes an explicit
+    causal limit ``j <= i + causal_offset`` (default S_k - S_q)."""
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _check_bf16(name, t)
+    B, Hq, S_q, D = q.shape
+    Bk, Hkv, S_k, Dk = k.shape
+    if tuple(v.shape) != tuple(k.shape) or Bk != B or Dk != D:
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if causal_offset is None:
+        causal_offset = S_k - S_q
+    mask_ptr = None
+    if block_mask is not None:
+        nQB, nKB = -(-S_q // blk), -(-S_k // blk)
+        if block_mask.dtype != torch.uint8 or tuple(block_mask.shape) != (B, Hq, nQB, nKB) \
+                or not block_mask.is_contiguous() or block_mask.device != q.device:
+            raise ValueError(f"block_mask must be a contiguous uint8 [{B}, {Hq}, {nQB}, {nKB}] on q's device")
+        mask_ptr = block_mask.data_ptr()
+    if out is None:
+        out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+    if lse is None:
+        lse = torch.empty((B, Hq, S_q), dtype=torch.float32, device=q.device)
+    if out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq, S_q) or not lse.is_contiguous():
+        raise ValueError("lse must be a contiguous float32 tensor [B, Hq, S_q]")
+    with torch.cuda.device(q.device):
+        st = _lib.load().steel_attn_fwd_ex(
+            q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(), lse.data_ptr(),
+            B, Hq, Hkv, S_q, S_k, D, blk, float(scale), 1 if causal else 0, int(causal_offset),
+            _stream_handle(stream))
+    _lib.check(st)
+    return out, lse
+
+
+def attn_merge(o_parts, lse_parts, *, out=None, lse_out=None, stream=None):
+    """Combine partial results over disjoint key sets: o_parts fp32
+    [n, ..., D] and lse_parts fp32 [n, ...] (stacked outputs of attn_fwd_lse)
+    -> (out [..., D], lse [...])."""
+    torch = _torch()
+    if o_parts.dtype != torch.float32 or lse_parts.dtype != torch.float32:
+        raise ValueError("o_parts and lse_parts must be float32")
+    if not o_parts.is_contiguous() or not lse_parts.is_contiguous():
+        raise ValueError("o_parts and lse_parts must be contiguous")
+    if tuple(o_parts.shape[:-1]) != tuple(lse_parts.shape):
+        raise ValueError("o_parts must be lse_parts' shape plus a last dimension D")
+    n, D = o_parts.shape[0], o_parts.shape[-1]
+    rows = lse_parts[0].numel()
+    if out is None:
+        out = torch.empty(o_parts.shape[1:], dtype=torch.float32, device=o_parts.device)
+    if lse_out is None:
+        lse_out = torch.empty(lse_parts.shape[1:], dtype=torch.float32, device=o_parts.device)
+    with torch.cuda.device(o_parts.device):
+        st = _lib.load().steel_attn_merge(o_parts.data_ptr(), lse_parts.data_ptr(), n, rows, D,
+                                          out.data_ptr(), lse_out.data_ptr(), _stream_handle(stream))
+    _lib.check(st)
+    return out, lse_out
+
+
 def attn_fwd_window(q, k, v, window_blocks: int, sink_blocks: int = 0, *,
                     scale: Optional[float] = None, causal: bool = True, blk: int = BLK, out=None,
                     stream=None):

@@ -60,6 +60,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_attn_plan_window.argtypes = [c_int] * 9 + [c_void_p, c_size_t, c_void_p]
     lib.steel_topk_block_mask.restype = c_int
     lib.steel_topk_block_mask.argtypes = [c_void_p, c_void_p] + [c_int] * 10 + [c_void_p, c_void_p]
+    lib.steel_attn_fwd_ex.restype = c_int
+    lib.steel_attn_fwd_ex.argtypes = [c_void_p] * 6 + [c_int] * 7 + [c_float, c_int, c_int, c_void_p]
+    lib.steel_attn_merge.restype = c_int
+    lib.steel_attn_merge.argtypes = [c_void_p, c_void_p, c_int, ctypes.c_longlong, c_int, c_void_p,
+                                     c_void_p, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

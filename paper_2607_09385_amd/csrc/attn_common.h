@@ -22,6 +22,7 @@ struct AttnArgs {
   const __bf16* k;
   const __bf16* v;
   float* out;
+  float* lse;               // [B][Hq][S_q] row log-sum-exp, or nullptr
   const int32_t* row_ptr;
   const uint32_t* col;
   const int32_t* order;

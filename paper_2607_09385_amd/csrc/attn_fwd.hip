@@ -396,6 +396,11 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
     const int qrow = qrow0 + 32 * nt;
     const float lt = half_pair_sum(l[nt]);
     const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    // log sum_j exp(scale s_ij) = (m + log2 l) ln 2: m in log2 units, l the
+    // row sum relative to 2^m (Algorithm 1's statistics)
+    if (a.lse != nullptr && hf == 0 && qrow < a.S_q)
+      a.lse[((size_t)b * a.Hq + head) * a.S_q + qrow] =
+          lt > 0.f ? (m[nt] + log2f(lt)) * 0.69314718055994531f : -INFINITY;
     if (qrow < a.S_q) {
       float* op = a.out + (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
 #pragma unroll
@@ -435,12 +440,14 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
 }
 
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
-                            float* out, float scale, const IndexBuffers& w, hipStream_t s) {
+                            float* out, float* lse, float scale, const IndexBuffers& w,
+                            hipStream_t s) {
   AttnArgs a;
   a.q = (const __bf16*)q;
   a.k = (const __bf16*)k;
   a.v = (const __bf16*)v;
   a.out = out;
+  a.lse = lse;
   a.row_ptr = w.row_ptr;
   a.col = w.col;
   a.order = nullptr;

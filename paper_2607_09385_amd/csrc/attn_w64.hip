@@ -579,6 +579,13 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
       for (int t = 0; t < 2; ++t) {
         const float lt = half_pair_sum(l[t]);
         const float inv = lt > 0.f ? 1.f / lt : 0.f;
+        // row log-sum-exp (m + log2 l) ln 2, one lane per row
+        if (a.lse != nullptr && hf == 0) {
+          const int qrow = cur.qb * kBlk + 32 * t + n;
+          if (qrow < a.S_q)
+            a.lse[((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q + qrow] =
+                lt > 0.f ? (m[t] + log2f(lt)) * 0.69314718055994531f : -INFINITY;
+        }
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
 #pragma unroll

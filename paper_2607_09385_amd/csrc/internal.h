@@ -79,8 +79,15 @@ hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, 
                             int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
                             hipStream_t stream);
 
-// Enqueue the fused attention over both item lists.
+// Enqueue the fused attention over both item lists; lse (nullable) receives
+// the row log-sum-exp [B][Hq][S_q].
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
-                            float* out, float scale, const IndexBuffers& w, hipStream_t stream);
+                            float* out, float* lse, float scale, const IndexBuffers& w,
+                            hipStream_t stream);
+
+// Enqueue the merge of n_parts partial results over disjoint key sets
+// (attn_merge.hip): o_parts [n_parts][rows][D], lse_parts [n_parts][rows].
+hipError_t launch_merge(const float* o_parts, const float* lse_parts, int n_parts, long long rows,
+                        int D, float* out, float* lse_out, hipStream_t stream);
 
 }  // namespace steel

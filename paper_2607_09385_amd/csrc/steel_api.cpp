@@ -198,7 +198,7 @@ int check_workspace(const void* ws, size_t bytes, const Layout& L) {
 // The fused call once the arguments are checked: stream-ordered workspace,
 // index build, attention, workspace release.
 int fused_call(const steel::Problem& p, const void* q, const void* k, const void* v,
-               const uint8_t* block_mask, void* out, float scale, void* stream) {
+               const uint8_t* block_mask, void* out, float* lse, float scale, void* stream) {
   int rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
@@ -213,7 +213,7 @@ int fused_call(const steel::Problem& p, const void* q, const void* k, const void
   const steel::IndexBuffers w = carve(ws, L);
   e = steel::launch_block_index(p, block_mask, w, s);
   if (e == hipSuccess)
-    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), scale, w, s);
+    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), lse, scale, w, s);
   hipError_t ef = hipFreeAsync(ws, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
@@ -236,7 +236,7 @@ int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* b
   int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
   if (rc != STEEL_OK) return rc;
   set_pack(&p);
-  return fused_call(p, q, k, v, block_mask, out, scale, stream);
+  return fused_call(p, q, k, v, block_mask, out, nullptr, scale, stream);
 }
 
 int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out, int B, int Hq,
@@ -248,7 +248,43 @@ int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out
   if (rc != STEEL_OK) return rc;
   if ((rc = set_window(&p, window_blocks, sink_blocks)) != STEEL_OK) return rc;
   set_pack(&p);
-  return fused_call(p, q, k, v, nullptr, out, scale, stream);
+  return fused_call(p, q, k, v, nullptr, out, nullptr, scale, stream);
+}
+
+int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t* block_mask,
+                      void* out, float* lse, int B, int Hq, int Hkv, int S_q, int S_k, int D,
+                      int blk, float scale, int causal, int causal_offset, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  if (causal) {
+    if (causal_offset < -(1 << 30) || causal_offset > (1 << 30))
+      return fail(STEEL_ERR_INVALID_ARGUMENT, "causal_offset %d outside [-2^30, 2^30]", causal_offset);
+    p.delta = causal_offset;
+  }
+  set_pack(&p);
+  return fused_call(p, q, k, v, block_mask, out, lse, scale, stream);
+}
+
+int steel_attn_merge(const float* o_parts, const float* lse_parts, int n_parts, long long rows,
+                     int D, float* out, float* lse_out, void* stream) {
+  g_err.clear();
+  if (!o_parts || !lse_parts || !out)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "o_parts, lse_parts and out must be non-NULL");
+  if (!aligned16(o_parts) || !aligned16(out))
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "o_parts and out must be 16-byte aligned");
+  if (n_parts < 1 || rows < 1)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "n_parts (%d) and rows (%lld) must be >= 1", n_parts,
+                rows);
+  if (D < 4 || D % 4 != 0)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "D=%d must be a positive multiple of 4", D);
+  if (rows * (D / 4) >= (1ll << 40))
+    return fail(STEEL_ERR_UNSUPPORTED, "%lld rows of %d values is too large", rows, D);
+  hipError_t e = steel::launch_merge(o_parts, lse_parts, n_parts, rows, D, out, lse_out,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "launching the merge");
+  return STEEL_OK;
 }
 
 size_t steel_attn_workspace_bytes(int B, int Hq, int Hkv, int S_q, int S_k, int blk) {
@@ -302,7 +338,7 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out, int B
   const Layout L = layout(p, true);
   if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
   hipError_t e = steel::launch_attention(
-      p, q, k, v, static_cast<float*>(out), scale,
+      p, q, k, v, static_cast<float*>(out), nullptr, scale,
       carve(const_cast<char*>(static_cast<const char*>(workspace)), L),
       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "launching the attention kernels");

@@ -163,3 +163,21 @@ def test_topk_block_mask_rejects_invalid():
     assert st == 2 and "4096" in _lib.last_error()
     st = lib.steel_topk_block_mask(FAKE, FAKE, 1, 3, 2, 128, 128, 64, 64, 1, 1, 10, FAKE, None)
     assert st == 1 and "multiple" in _lib.last_error()
+
+
+def test_lse_and_merge_entry_points_reject_invalid():
+    lib = _lib.load()
+    st = lib.steel_attn_fwd_ex(FAKE, FAKE, FAKE, None, FAKE, FAKE, 1, 4, 2, 128, 128, 96, 64, 0.1, 1,
+                               0, None)
+    assert st == 2 and "D=96" in _lib.last_error()
+    st = lib.steel_attn_fwd_ex(FAKE, FAKE, FAKE, None, None, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.1, 1,
+                               0, None)
+    assert st == 1 and "non-NULL" in _lib.last_error()
+    st = lib.steel_attn_merge(FAKE, FAKE, 0, 10, 64, FAKE, None, None)
+    assert st == 1 and "n_parts" in _lib.last_error()
+    st = lib.steel_attn_merge(FAKE, FAKE, 2, 10, 66, FAKE, None, None)
+    assert st == 1 and "multiple of 4" in _lib.last_error()
+    st = lib.steel_attn_merge(None, FAKE, 2, 10, 64, FAKE, None, None)
+    assert st == 1 and "non-NULL" in _lib.last_error()
+    st = lib.steel_attn_merge(FAKE + 4, FAKE, 2, 10, 64, FAKE, None, None)
+    assert st == 1 and "aligned" in _lib.last_error()
