@@ -434,6 +434,7 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
       launch_attention_w64(ap, s);
     else launch_one<D, 4>(ap, p.NP, s);
   }
+  if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item
   a.order = w.order_s;
   a.n_items = w.n_items;
   launch_one<D, 1>(a, p.R, s);

@@ -37,6 +37,10 @@ struct Problem {
   // core rather than fetching them, Section III-B; windowed attention is the
   // masking scheme Section IV-A names).
   int win_blocks, sink_blocks;
+  // Set by the fused calls when every query head has the same block mask (no
+  // mask tensor, or the structured mask): with pack > 1 every head pack is
+  // then uniform and the single-head list is empty, so it is not launched.
+  int heads_share_mask;
 };
 
 // Device workspace of one call.

@@ -236,6 +236,7 @@ int steel_attn_fwd(const void* q, const void* k, const void* v, const uint8_t* b
   int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
   if (rc != STEEL_OK) return rc;
   set_pack(&p);
+  p.heads_share_mask = block_mask == nullptr;
   return fused_call(p, q, k, v, block_mask, out, nullptr, scale, stream);
 }
 
@@ -248,6 +249,7 @@ int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out
   if (rc != STEEL_OK) return rc;
   if ((rc = set_window(&p, window_blocks, sink_blocks)) != STEEL_OK) return rc;
   set_pack(&p);
+  p.heads_share_mask = 1;
   return fused_call(p, q, k, v, nullptr, out, nullptr, scale, stream);
 }
 
@@ -264,6 +266,7 @@ int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t
     p.delta = causal_offset;
   }
   set_pack(&p);
+  p.heads_share_mask = block_mask == nullptr;
   return fused_call(p, q, k, v, block_mask, out, lse, scale, stream);
 }
 
