@@ -259,6 +259,7 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
     # window/sink workloads: the same call with the mask generated from block
     # coordinates (no mask tensor read by the index build)
     structured = None
+    structured_b16 = None
     if cfg.mask == "window_sink":
         def step_w():
             steel.attn_fwd_window(qd, kd, vd, cfg.window_blocks, cfg.sink_blocks, scale=cfg.scale,
@@ -273,6 +274,24 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
         wall_w = (time.perf_counter() - t0) / steps
         structured = {"call": "steel_attn_fwd_window", "ms_per_step": round(wall_w * 1e3, 4),
                       "effective_tflops": round(f_live / wall_w / 1e12, 2)}
+        # the same call with the output in bf16 (half the output bytes)
+        out16 = torch.empty((cfg.B, cfg.Hq, cfg.S_q, cfg.D), dtype=torch.bfloat16, device=dev)
+        lse16 = torch.empty((cfg.B, cfg.Hq, cfg.S_q), dtype=torch.float32, device=dev)
+
+        def step_b():
+            steel.attn_fwd_lse(qd, kd, vd, md, scale=cfg.scale, causal=cfg.causal, out=out16,
+                               lse=lse16, out_dtype=torch.bfloat16)
+        for _ in range(warmup):
+            step_b()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step_b()
+        torch.cuda.synchronize()
+        wall_b = (time.perf_counter() - t0) / steps
+        structured_b16 = {"call": "steel_attn_fwd_ex (bf16 output, with lse)",
+                          "ms_per_step": round(wall_b * 1e3, 4),
+                          "effective_tflops": round(f_live / wall_b / 1e12, 2)}
     line = {
         "metric": METRIC,
         "value": round(f_live / wall / 1e12, 2),
@@ -330,6 +349,8 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu):
                                  "algorithmic_bytes": nbytes}}
     if structured is not None:
         line["structured_mask"] = structured
+    if structured_b16 is not None:
+        line["bf16_output"] = structured_b16
     if producer is not None:
         line["mask_producer"] = producer
     if want_cpu:

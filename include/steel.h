@@ -146,14 +146,19 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out,
  *                  a chunk [k0, k1) of a sequence of S_k_total keys is passed
  *                  as its own K, V with causal_offset = S_k_total - S_q - k0.
  *                  Ignored when causal == 0; otherwise within [-2^30, 2^30].
+ *   out_bf16       0: out is fp32 [B][Hq][S_q][D] (as steel_attn_fwd);
+ *                  1: out is bf16, each value the round-to-nearest-even of
+ *                  the fp32 result (half the output bytes; the error budget
+ *                  of this form is larger, see the library's design notes).
  *
- * Everything else as steel_attn_fwd; with lse == NULL and causal_offset =
- * S_k - S_q the output is bitwise that of steel_attn_fwd.
+ * Everything else as steel_attn_fwd; with lse == NULL, causal_offset =
+ * S_k - S_q and out_bf16 == 0 the output is bitwise that of steel_attn_fwd.
  */
 int steel_attn_fwd_ex(const void* q, const void* k, const void* v,
                       const uint8_t* block_mask, void* out, float* lse,
                       int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
-                      float scale, int causal, int causal_offset, void* stream);
+                      float scale, int causal, int causal_offset, int out_bf16,
+                      void* stream);
 
 /*
  * Merge of partial results over disjoint key sets: with n_parts outputs O_c

@@ -89,10 +89,12 @@ def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal:
 
 def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal: bool = True,
                  causal_offset: Optional[int] = None, blk: int = BLK, out=None, lse=None,
-                 stream=None):
+                 out_dtype=None, stream=None):
     """``attn_fwd`` that also returns the row log-sum-exp (fp32 [B, Hq, S_q],
     natural log, -inf for rows with no visible key) and takes an explicit
-    causal limit ``j <= i + causal_offset`` (default S_k - S_q)."""
+    causal limit ``j <= i + causal_offset`` (default S_k - S_q).  ``out_dtype``
+    torch.float32 (default) or torch.bfloat16 (the fp32 result rounded to
+    nearest even)."""
     torch = _torch()
     for name, t in (("q", q), ("k", k), ("v", v)):
         _check_bf16(name, t)
@@ -111,19 +113,22 @@ def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, cau
                 or not block_mask.is_contiguous() or block_mask.device != q.device:
             raise ValueError(f"block_mask must be a contiguous uint8 [{B}, {Hq}, {nQB}, {nKB}] on q's device")
         mask_ptr = block_mask.data_ptr()
+    odt = torch.float32 if out_dtype is None else out_dtype
+    if odt not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
     if out is None:
-        out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+        out = torch.empty((B, Hq, S_q, D), dtype=odt, device=q.device)
     if lse is None:
         lse = torch.empty((B, Hq, S_q), dtype=torch.float32, device=q.device)
-    if out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
-        raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+    if out.dtype != odt or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous {odt} tensor [B, Hq, S_q, D]")
     if lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq, S_q) or not lse.is_contiguous():
         raise ValueError("lse must be a contiguous float32 tensor [B, Hq, S_q]")
     with torch.cuda.device(q.device):
         st = _lib.load().steel_attn_fwd_ex(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(), lse.data_ptr(),
             B, Hq, Hkv, S_q, S_k, D, blk, float(scale), 1 if causal else 0, int(causal_offset),
-            _stream_handle(stream))
+            1 if odt == torch.bfloat16 else 0, _stream_handle(stream))
     _lib.check(st)
     return out, lse
 

@@ -61,7 +61,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_topk_block_mask.restype = c_int
     lib.steel_topk_block_mask.argtypes = [c_void_p, c_void_p] + [c_int] * 10 + [c_void_p, c_void_p]
     lib.steel_attn_fwd_ex.restype = c_int
-    lib.steel_attn_fwd_ex.argtypes = [c_void_p] * 6 + [c_int] * 7 + [c_float, c_int, c_int, c_void_p]
+    lib.steel_attn_fwd_ex.argtypes = [c_void_p] * 6 + [c_int] * 7 + [c_float, c_int, c_int, c_int,
+                                                                     c_void_p]
     lib.steel_attn_merge.restype = c_int
     lib.steel_attn_merge.argtypes = [c_void_p, c_void_p, c_int, ctypes.c_longlong, c_int, c_void_p,
                                      c_void_p, c_void_p]

@@ -10,6 +10,7 @@
 namespace steel {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -23,6 +24,7 @@ struct AttnArgs {
   const __bf16* v;
   float* out;
   float* lse;               // [B][Hq][S_q] row log-sum-exp, or nullptr
+  int out_bf16;             // out holds bf16 (round to nearest even), not fp32
   const int32_t* row_ptr;
   const uint32_t* col;
   const int32_t* order;

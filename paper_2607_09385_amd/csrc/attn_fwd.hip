@@ -402,14 +402,19 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
       a.lse[((size_t)b * a.Hq + head) * a.S_q + qrow] =
           lt > 0.f ? (m[nt] + log2f(lt)) * 0.69314718055994531f : -INFINITY;
     if (qrow < a.S_q) {
-      float* op = a.out + (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
+      const size_t at = (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
           f32x4 w = {o[nt][dt][4 * gq] * inv, o[nt][dt][4 * gq + 1] * inv,
                      o[nt][dt][4 * gq + 2] * inv, o[nt][dt][4 * gq + 3] * inv};
-          *(f32x4*)(op + 32 * dt + 8 * gq) = w;
+          if (a.out_bf16) {
+            const bf16x4 wb = {(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
+            *(bf16x4*)((__bf16*)a.out + at + 32 * dt + 8 * gq) = wb;
+          } else {
+            *(f32x4*)(a.out + at + 32 * dt + 8 * gq) = w;
+          }
         }
     }
   }
@@ -449,6 +454,7 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.v = (const __bf16*)v;
   a.out = out;
   a.lse = lse;
+  a.out_bf16 = p.out_bf16;
   a.row_ptr = w.row_ptr;
   a.col = w.col;
   a.order = nullptr;

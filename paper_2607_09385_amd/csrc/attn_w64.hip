@@ -573,7 +573,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
     {
       char* const stg = (char*)smem + stage_bytes((pos + L + 3 + (wave >> 1)) % ST) +
                         (uint32_t)(wave & 1) * 16384u;
-      float* const ob = a.out + ((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q * D;
+      const size_t ob = ((size_t)cur.b * a.Hq + cur.h0 + wave) * a.S_q * D;  // element offset
       const int rr = lane >> 5, cc = lane & 31;  // read-back: row 2k + rr, chunk cc
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
@@ -604,14 +604,27 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
             const int r = 2 * k + rr;
             w[k] = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
           }
+          if (a.out_bf16) {
 #pragma unroll
-          for (int k = 0; k < 16; ++k) *(f32x4*)(ob + (size_t)(qrow0 + 2 * k + rr) * D + 4 * cc) = w[k];
+            for (int k = 0; k < 16; ++k)
+              *(bf16x4*)((__bf16*)a.out + ob + (size_t)(qrow0 + 2 * k + rr) * D + 4 * cc) =
+                  bf16x4{(__bf16)w[k][0], (__bf16)w[k][1], (__bf16)w[k][2], (__bf16)w[k][3]};
+          } else {
+#pragma unroll
+            for (int k = 0; k < 16; ++k) *(f32x4*)(a.out + ob + (size_t)(qrow0 + 2 * k + rr) * D + 4 * cc) = w[k];
+          }
         } else {
 #pragma unroll
           for (int k = 0; k < 16; ++k) {
             const int r = 2 * k + rr;
             const f32x4 w = *(const f32x4*)(stg + r * 512 + ((cc ^ r) << 4));
-            if (qrow0 + r < a.S_q) *(f32x4*)(ob + (size_t)(qrow0 + r) * D + 4 * cc) = w;
+            if (qrow0 + r < a.S_q) {
+              const size_t at = ob + (size_t)(qrow0 + r) * D + 4 * cc;
+              if (a.out_bf16)
+                *(bf16x4*)((__bf16*)a.out + at) = bf16x4{(__bf16)w[0], (__bf16)w[1], (__bf16)w[2], (__bf16)w[3]};
+              else
+                *(f32x4*)(a.out + at) = w;
+            }
           }
         }
 #pragma unroll

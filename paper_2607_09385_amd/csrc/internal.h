@@ -41,6 +41,7 @@ struct Problem {
   // mask tensor, or the structured mask): with pack > 1 every head pack is
   // then uniform and the single-head list is empty, so it is not launched.
   int heads_share_mask;
+  int out_bf16;  // output in bf16 (RNE of the fp32 result) instead of fp32
 };
 
 // Device workspace of one call.

@@ -255,7 +255,8 @@ int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out
 
 int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t* block_mask,
                       void* out, float* lse, int B, int Hq, int Hkv, int S_q, int S_k, int D,
-                      int blk, float scale, int causal, int causal_offset, void* stream) {
+                      int blk, float scale, int causal, int causal_offset, int out_bf16,
+                      void* stream) {
   g_err.clear();
   steel::Problem p{};
   int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
@@ -265,6 +266,9 @@ int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t
       return fail(STEEL_ERR_INVALID_ARGUMENT, "causal_offset %d outside [-2^30, 2^30]", causal_offset);
     p.delta = causal_offset;
   }
+  if (out_bf16 != 0 && out_bf16 != 1)
+    return fail(STEEL_ERR_INVALID_ARGUMENT, "out_bf16 must be 0 or 1 (got %d)", out_bf16);
+  p.out_bf16 = out_bf16;
   set_pack(&p);
   p.heads_share_mask = block_mask == nullptr;
   return fused_call(p, q, k, v, block_mask, out, lse, scale, stream);
