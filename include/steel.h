@@ -28,8 +28,11 @@
  * surface at the caller's next synchronisation, as usual for HIP.
  *
  * Thread safety: calls may be made concurrently from several threads and on
- * several streams; the only process-wide state is a per-device memory pool
- * for internal workspace and the thread-local error text.
+ * several streams; the only process-wide state is one internal scratch
+ * buffer per device and the thread-local error text.  Calls that use the
+ * scratch buffer take turns while they enqueue (a short host lock) and are
+ * ordered on the GPU by an event, so calls on different streams of one
+ * device run one after the other.
  */
 #ifndef STEEL_H
 #define STEEL_H
@@ -66,8 +69,10 @@ typedef enum steel_status {
  *
  * Inputs and output are owned by the caller; the library keeps no pointer to
  * them after it returns.  Internal workspace (the compressed live-block list
- * and the work order) is taken stream-ordered from a per-device pool and
- * released stream-ordered.  Results are bitwise reproducible run to run.
+ * and the work order) lives in the device's scratch buffer, which the library
+ * allocates on first use and grows (hipMalloc, synchronous) when a call needs
+ * more than it holds; it is kept until the process ends.  Results are bitwise
+ * reproducible run to run.
  */
 int steel_attn_fwd(const void* q, const void* k, const void* v,
                    const uint8_t* block_mask, void* out,
@@ -234,9 +239,9 @@ int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, in
  *   keep_num, keep_den   1 <= keep_num <= keep_den (1 and 10: 10%)
  *   block_mask  uint8 device buffer of B*Hq*nQB*nKB bytes, caller-owned
  *
- * Float64 workspace for the block means and scores is taken stream-ordered
- * from the per-device pool and released stream-ordered; the call only
- * enqueues.  Errors as for steel_attn_fwd.
+ * Float64 workspace for the block means and scores lives in the device's
+ * scratch buffer (as for steel_attn_fwd); the call only enqueues, unless the
+ * buffer must grow.  Errors as for steel_attn_fwd.
  */
 int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, int S_q,
                           int S_k, int D, int blk, int causal, int keep_num, int keep_den,

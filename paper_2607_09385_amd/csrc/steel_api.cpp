@@ -38,30 +38,81 @@ int hip_fail(hipError_t e, const char* what) {
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 constexpr int kMaxDevices = 64;
-std::mutex g_pool_mu;
-hipMemPool_t g_pools[kMaxDevices] = {};
 
-hipError_t device_pool(int dev, hipMemPool_t* out) {
-  std::lock_guard<std::mutex> lk(g_pool_mu);
-  if (!g_pools[dev]) {
-    hipMemPoolProps props = {};
-    props.allocType = hipMemAllocationTypePinned;
-    props.handleTypes = hipMemHandleTypeNone;
-    props.location.type = hipMemLocationTypeDevice;
-    props.location.id = dev;
-    hipMemPool_t pool = nullptr;
-    hipError_t e = hipMemPoolCreate(&pool, &props);
-    if (e != hipSuccess) return e;
-    uint64_t keep = UINT64_MAX;
-    e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-    if (e != hipSuccess) {
-      (void)hipMemPoolDestroy(pool);
-      return e;
-    }
-    g_pools[dev] = pool;
+// Internal scratch (the live-block index of a fused call, the means and
+// scores of the mask producer): one buffer per device, kept for the life of
+// the process and grown when a call needs more.  A stream-ordered pool
+// allocation per call made every call wait on the host for the previous one
+// (the runtime waits for the block's release), so calls could not be queued
+// ahead.  Reuse is ordered on the GPU instead: each call makes its stream wait
+// for the completion event of the previous user of the buffer and records its
+// own; host threads take turns while they enqueue (the lock is held from
+// scratch_begin to scratch_end).
+struct DeviceScratch {
+  std::mutex mu;
+  char* ptr = nullptr;
+  size_t bytes = 0;
+  hipEvent_t done = nullptr;  // completion of the last call that used ptr
+  bool recorded = false;
+};
+DeviceScratch g_scratch[kMaxDevices];
+
+// Selects dev for the calls in its scope and restores the caller's device.
+struct DeviceScope {
+  int prev = -1;
+  hipError_t err = hipSuccess;
+  explicit DeviceScope(int dev) {
+    err = hipGetDevice(&prev);
+    if (err == hipSuccess && prev != dev) err = hipSetDevice(dev);
   }
-  *out = g_pools[dev];
-  return hipSuccess;
+  ~DeviceScope() {
+    if (prev >= 0) (void)hipSetDevice(prev);
+  }
+};
+
+int scratch_begin(int dev, hipStream_t s, size_t need, std::unique_lock<std::mutex>* lk,
+                  char** out) {
+  DeviceScratch& d = g_scratch[dev];
+  *lk = std::unique_lock<std::mutex>(d.mu);
+  DeviceScope scope(dev);
+  if (scope.err != hipSuccess) return hip_fail(scope.err, "selecting the stream's device");
+  hipError_t e = hipSuccess;
+  if (!d.done && (e = hipEventCreateWithFlags(&d.done, hipEventDisableTiming)) != hipSuccess)
+    return hip_fail(e, "creating the scratch event");
+  if (need > d.bytes) {
+    if (d.ptr) {
+      if (d.recorded && (e = hipEventSynchronize(d.done)) != hipSuccess)
+        return hip_fail(e, "waiting for the previous user of the scratch buffer");
+      if ((e = hipFree(d.ptr)) != hipSuccess) return hip_fail(e, "releasing the scratch buffer");
+      d.ptr = nullptr;
+      d.bytes = 0;
+      d.recorded = false;
+    }
+    const size_t grow = (need + need / 4 + ((size_t)1 << 20) - 1) & ~(((size_t)1 << 20) - 1);
+    if ((e = hipMalloc(reinterpret_cast<void**>(&d.ptr), grow)) != hipSuccess) {
+      d.ptr = nullptr;
+      return hip_fail(e, "allocating the scratch buffer");
+    }
+    d.bytes = grow;
+  }
+  if (d.recorded && (e = hipStreamWaitEvent(s, d.done, 0)) != hipSuccess)
+    return hip_fail(e, "ordering after the previous user of the scratch buffer");
+  *out = d.ptr;
+  return STEEL_OK;
+}
+
+// After the call's work is enqueued on s (lock still held).
+int scratch_end(int dev, hipStream_t s) {
+  DeviceScratch& d = g_scratch[dev];
+  DeviceScope scope(dev);
+  if (scope.err != hipSuccess) return hip_fail(scope.err, "selecting the stream's device");
+  hipError_t e = hipEventRecord(d.done, s);
+  if (e != hipSuccess) {
+    d.recorded = false;
+    return hip_fail(e, "recording the scratch buffer's use");
+  }
+  d.recorded = true;
+  return STEEL_OK;
 }
 
 // Shape checks shared by both entry points; fills the Problem on success.
@@ -195,29 +246,25 @@ int check_workspace(const void* ws, size_t bytes, const Layout& L) {
   return STEEL_OK;
 }
 
-// The fused call once the arguments are checked: stream-ordered workspace,
-// index build, attention, workspace release.
+// The fused call once the arguments are checked: the device's scratch buffer,
+// index build, attention.
 int fused_call(const steel::Problem& p, const void* q, const void* k, const void* v,
                const uint8_t* block_mask, void* out, float* lse, float scale, void* stream) {
   int rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
-  hipMemPool_t pool;
-  hipError_t e = device_pool(dev, &pool);
-  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
   const Layout L = layout(p, true);
+  std::unique_lock<std::mutex> lk;
   char* ws = nullptr;
-  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), L.total, pool, s);
-  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
+  if ((rc = scratch_begin(dev, s, L.total, &lk, &ws)) != STEEL_OK) return rc;
   const steel::IndexBuffers w = carve(ws, L);
-  e = steel::launch_block_index(p, block_mask, w, s);
+  hipError_t e = steel::launch_block_index(p, block_mask, w, s);
   if (e == hipSuccess)
     e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), lse, scale, w, s);
-  hipError_t ef = hipFreeAsync(ws, s);
+  const int re = scratch_end(dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
-  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
-  return STEEL_OK;
+  return re;
 }
 
 }  // namespace
@@ -373,24 +420,20 @@ int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, 
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
-  hipMemPool_t pool;
-  hipError_t e = device_pool(dev, &pool);
-  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
   const size_t n_qm = (size_t)B * Hq * p.nQB * D, n_km = (size_t)B * Hkv * p.nKB * D;
   const size_t n_sc = (size_t)B * Hq * p.nQB * p.nKB;
   const size_t o_km = align256(n_qm * sizeof(double)), o_sc = o_km + align256(n_km * sizeof(double));
   const size_t total = o_sc + align256(n_sc * sizeof(double));
+  std::unique_lock<std::mutex> lk;
   char* ws = nullptr;
-  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), total, pool, s);
-  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
-  e = steel::launch_topk_mask(p, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k),
-                              keep_num, keep_den, block_mask, reinterpret_cast<double*>(ws),
-                              reinterpret_cast<double*>(ws + o_km), reinterpret_cast<double*>(ws + o_sc),
-                              s);
-  hipError_t ef = hipFreeAsync(ws, s);
+  if ((rc = scratch_begin(dev, s, total, &lk, &ws)) != STEEL_OK) return rc;
+  hipError_t e = steel::launch_topk_mask(
+      p, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), keep_num, keep_den,
+      block_mask, reinterpret_cast<double*>(ws), reinterpret_cast<double*>(ws + o_km),
+      reinterpret_cast<double*>(ws + o_sc), s);
+  const int re = scratch_end(dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
-  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
-  return STEEL_OK;
+  return re;
 }
 
 int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k, int blk,
@@ -406,13 +449,10 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   hipStream_t s = static_cast<hipStream_t>(stream);
   int dev = 0;
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
-  hipMemPool_t pool;
-  hipError_t e = device_pool(dev, &pool);
-  if (e != hipSuccess) return hip_fail(e, "creating the workspace pool");
   const Layout L = layout(p, false);
+  std::unique_lock<std::mutex> lk;
   char* ws = nullptr;
-  e = hipMallocFromPoolAsync(reinterpret_cast<void**>(&ws), L.total, pool, s);
-  if (e != hipSuccess) return hip_fail(e, "allocating workspace");
+  if ((rc = scratch_begin(dev, s, L.total, &lk, &ws)) != STEEL_OK) return rc;
   steel::IndexBuffers w;
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
@@ -422,11 +462,10 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   w.row_ptr = row_ptr;
   w.col = col;
   w.order_s = order;
-  e = steel::launch_block_index(p, block_mask, w, s);
-  hipError_t ef = hipFreeAsync(ws, s);
+  hipError_t e = steel::launch_block_index(p, block_mask, w, s);
+  const int re = scratch_end(dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
-  if (ef != hipSuccess) return hip_fail(ef, "releasing workspace");
-  return STEEL_OK;
+  return re;
 }
 
 }  // extern "C"
