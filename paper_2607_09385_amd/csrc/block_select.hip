@@ -16,8 +16,10 @@
 //                 staged in LDS, one thread per column
 //   block_scores  64 x 64 score tiles per workgroup from LDS-staged means
 //                 (tiles above the diagonal skipped when causal)
-//   topk_select   one wave per (head, query block): bitonic sort of the
-//                 candidates in LDS, then the mask row
+//   topk_select   one wave per (head, query block): a radix select over
+//                 order-preserving integer keys of the scores (rows of up to
+//                 512 key blocks), or a bitonic sort of the candidates in
+//                 LDS (longer rows), then the mask row
 #include <algorithm>
 #include <climits>
 
@@ -190,6 +192,97 @@ __global__ __launch_bounds__(256) void k_topk_select(const double* __restrict__ 
   for (int kb = lane; kb < nKB; kb += 64) dst[kb] = flag[kb];
 }
 
+// Rows of at most 64 * kSelPerLane key blocks: a radix select in registers.
+// Each score becomes an unsigned key in the order of the doubles (both zeros
+// give the key of +0, so equal scores give equal keys).  Eight passes, one
+// byte each from the top, narrow down the key of the keep-th largest score
+// with a 256-bin histogram per wave in LDS; every candidate with a larger
+// key is kept, and of those with that key the ones with the smallest key
+// block indices, as many as are still missing.  The result is the same set
+// as a full sort by (score descending, kb ascending).
+constexpr int kSelPerLane = 8;
+
+__device__ __forceinline__ uint64_t order_key(double x) {
+  if (x == 0.0) x = 0.0;  // -0 and +0 compare equal
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+__global__ __launch_bounds__(256) void k_topk_select_radix(const double* __restrict__ scores,
+                                                           int nQB, int nKB, int causal,
+                                                           long long keep_num, long long keep_den,
+                                                           long long n_rows,
+                                                           uint8_t* __restrict__ mask) {
+  __shared__ unsigned hist_all[4][256];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const long long row = (long long)blockIdx.x * 4 + w;  // (b*Hq + h)*nQB + qb
+  if (row >= n_rows) return;  // the whole wave; no workgroup barrier follows
+  unsigned* hist = hist_all[w];
+  const int qb = (int)(row % nQB);
+  const int ncand = causal ? min(qb + 1, nKB) : nKB;
+  int need = (int)((keep_num * ncand + keep_den - 1) / keep_den);
+  const double* src = scores + (size_t)row * nKB;
+  uint64_t key[kSelPerLane];  // 0: not a candidate (below every score's key)
+#pragma unroll
+  for (int c = 0; c < kSelPerLane; ++c) {
+    const int j = lane + 64 * c;
+    key[c] = j < ncand ? order_key(src[j]) : 0ull;
+  }
+  uint64_t prefix = 0;  // the bytes of the boundary key found so far
+#pragma unroll 1
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) hist[4 * lane + i] = 0u;
+    wave_lds_sync();
+#pragma unroll
+    for (int c = 0; c < kSelPerLane; ++c)
+      if (key[c] != 0ull && ((key[c] >> shift) >> 8) == prefix)  // higher bytes match
+        atomicAdd(&hist[(unsigned)(key[c] >> shift) & 255u], 1u);
+    wave_lds_sync();
+    // bins 4*lane .. 4*lane+3; counts of the higher bins come from the
+    // lanes above (a suffix sum over the wave)
+    unsigned h[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) h[i] = hist[4 * lane + i];
+    const unsigned tot = h[0] + h[1] + h[2] + h[3];
+    unsigned suf = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned t = __shfl_down(suf, o);
+      if (lane + o < 64) suf += t;
+    }
+    unsigned above = suf - tot;
+    int found = -1;
+    unsigned found_above = 0;
+#pragma unroll
+    for (int i = 3; i >= 0; --i) {
+      if (found < 0 && above < (unsigned)need && above + h[i] >= (unsigned)need) {
+        found = 4 * lane + i;
+        found_above = above;
+      }
+      above += h[i];
+    }
+    // exactly one bin holds the need-th largest remaining key
+    const int src_lane = __builtin_ctzll(__ballot(found >= 0));
+    const int v = __shfl(found, src_lane);
+    need -= (int)__shfl(found_above, src_lane);
+    prefix = (prefix << 8) | (uint64_t)v;
+  }
+  uint8_t* dst = mask + (size_t)row * nKB;
+  int eq_before = 0;  // candidates with the boundary key in earlier lane groups
+#pragma unroll
+  for (int c = 0; c < kSelPerLane; ++c) {
+    const int j = lane + 64 * c;
+    const bool eq = key[c] == prefix;
+    const uint64_t m = __ballot(eq);
+    const int rank = eq_before + __popcll(m & ((1ull << lane) - 1ull));
+    const bool keep = key[c] > prefix || (eq && rank < need) || j == qb;
+    eq_before += __popcll(m);
+    if (j < nKB) dst[j] = keep ? 1 : 0;
+  }
+}
+
 hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, int keep_num,
                             int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
                             hipStream_t s) {
@@ -200,11 +293,17 @@ hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, 
                      p.D, km);
   hipLaunchKernelGGL(k_block_scores, dim3(p.B * p.Hq * ntq * ntk), dim3(256), 0, s, qm, km, p.nQB,
                      p.nKB, p.D, p.G, p.Hq, p.Hkv, p.causal, ntq, ntk, scores);
+  const long long rows = (long long)p.B * p.Hq * p.nQB;
+  if (p.nKB <= 64 * kSelPerLane) {
+    hipLaunchKernelGGL(k_topk_select_radix, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s,
+                       scores, p.nQB, p.nKB, p.causal, (long long)keep_num, (long long)keep_den,
+                       rows, mask);
+    return hipGetLastError();
+  }
   int n2max = 1;
   while (n2max < p.nKB) n2max <<= 1;
   const size_t seg = (12 * (size_t)n2max + (size_t)p.nKB + 15) & ~(size_t)15;  // per wave
   const int wpg = (int)std::max<size_t>(1, std::min<size_t>(4, 65536 / seg));   // waves per group
-  const long long rows = (long long)p.B * p.Hq * p.nQB;
   hipLaunchKernelGGL(k_topk_select, dim3((unsigned)((rows + wpg - 1) / wpg)), dim3(64 * wpg),
                      wpg * seg, s, scores, p.nQB, p.nKB, n2max, seg, p.causal, (long long)keep_num,
                      (long long)keep_den, rows, mask);
