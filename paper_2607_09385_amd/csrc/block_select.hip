@@ -60,6 +60,7 @@ __global__ __launch_bounds__(256) void k_block_scores(const double* __restrict__
                                                       double* __restrict__ scores) {
 #pragma clang fp contract(off)
   constexpr int DC = 32;  // d chunk staged in LDS
+  static_assert(kBlk * DC % 256 == 0, "whole staging rounds");
   // rows padded by 2 doubles: the staging writes step over banks and every row
   // stays 16-byte aligned for the paired operand reads
   __shared__ __attribute__((aligned(16))) double qs[DC][kBlk + 2];
@@ -81,12 +82,24 @@ __global__ __launch_bounds__(256) void k_block_scores(const double* __restrict__
 #pragma unroll
     for (int c = 0; c < 4; ++c) acc[a][c] = 0.0;
   for (int d0 = 0; d0 < D; d0 += DC) {
-    // stage qm / km rows of the tile, d-major
-    for (int e = t; e < kBlk * DC; e += 256) {
+    // stage qm / km rows of the tile, d-major: every load is issued before
+    // the first LDS write, so their latencies overlap
+    constexpr int PER = kBlk * DC / 256;
+    double qv[PER], kv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = t + 256 * u;
       const int r = e / DC, dd = e - r * DC;
       const int qb = tq * kBlk + r, kb = tk * kBlk + r;
-      qs[dd][r] = qb < nQB ? qrow[(size_t)qb * D + d0 + dd] : 0.0;
-      ks[dd][r] = kb < nKB ? krow[(size_t)kb * D + d0 + dd] : 0.0;
+      qv[u] = qb < nQB ? qrow[(size_t)qb * D + d0 + dd] : 0.0;
+      kv[u] = kb < nKB ? krow[(size_t)kb * D + d0 + dd] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = t + 256 * u;
+      const int r = e / DC, dd = e - r * DC;
+      qs[dd][r] = qv[u];
+      ks[dd][r] = kv[u];
     }
     __syncthreads();
     // operands of step dd + 1 are read while step dd computes
