@@ -107,7 +107,10 @@ __device__ __forceinline__ void mfma_acc(f32x16& acc, const bf16x8& a, const bf1
 
 }  // namespace
 
-template <int D>
+// RAGGED: S_k is not a multiple of the block, so the last key block is cut
+// short and its copies clamp their rows.  Without it that path is compiled
+// out (its address arithmetic would otherwise run on every tile).
+template <int D, bool RAGGED>
 __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   constexpr int NW = 4;             // waves = query heads of the pack
   constexpr int C = D / 8;          // 16-byte chunks per row
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   const uint32_t co0 = cp_off(0), co1 = cp_off(1), co2 = cp_off(2), co3 = cp_off(3);
   auto issue_copy = [&](const __bf16* src, uint32_t dst, int kb) __attribute__((always_inline)) {
     const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW) * 1024u;
-    if ((kb + 1) * kBlk <= a.S_k) {
+    if (!RAGGED || (kb + 1) * kBlk <= a.S_k) {
       // the item's pointers may sit in VGPRs: the base goes to an SGPR pair
       const uint64_t p = (uint64_t)(uintptr_t)(src + (size_t)kb * kBlk * D);
       const uint64_t ps = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
@@ -653,7 +656,10 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
 }
 
 hipError_t launch_attention_w64(const AttnArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_attn_w64<128>, dim3(256), dim3(256), 0, s, a);
+  if (a.S_k % kBlk != 0)
+    hipLaunchKernelGGL((k_attn_w64<128, true>), dim3(256), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_attn_w64<128, false>), dim3(256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
