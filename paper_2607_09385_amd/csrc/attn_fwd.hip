@@ -62,7 +62,9 @@ constexpr int nt_for() { return STEEL_NT; }
 // N-tiles of one head: NT = 2 (one wave per head; every K/V fragment read from
 // LDS feeds two MFMAs; the wave needs most of the register file) or NT = 1
 // (two waves per head, half the registers, so two waves share a SIMD).
-template <int D, int PACK, int NT>
+// RAGGED: S_k is not a multiple of the block (the tail block's copies clamp
+// their rows); without it that path is compiled out.
+template <int D, int PACK, int NT, bool RAGGED>
 __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
   constexpr int WPH = 2 / NT;      // waves per head
   constexpr int NW = PACK * WPH;   // waves
@@ -123,7 +125,7 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
   // dst.  Rows past S_k (the tail block) read the last key row instead.
   auto issue_copy = [&](const __bf16* src, uint32_t dst, int kb) {
     const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW) * 1024u;
-    if ((kb + 1) * kBlk <= a.S_k) {
+    if (!RAGGED || (kb + 1) * kBlk <= a.S_k) {
       const __bf16* sb = src + (size_t)kb * kBlk * D;
 #pragma unroll
       for (int j = 0; j < LPW; ++j) copy16_to_lds(sb, cp_off[j], lbase + j * 1024u);
@@ -423,9 +425,17 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
 template <int D, int PACK>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   constexpr int NT = nt_for<D>();
-  if (grid > 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, NT>), dim3(xcd_grid(grid)), dim3(64 * PACK * (2 / NT)), 0,
-                       s, a);
+  if (grid <= 0) return;
+  // At D = 64 the copy of the kernel without the ragged path needs fewer
+  // registers (162 vs 178), so a third wave fits on each SIMD, and it ran
+  // 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps the one
+  // variant.
+  if (D == 64 || a.S_k % kBlk != 0)
+    hipLaunchKernelGGL((k_attn<D, PACK, NT, true>), dim3(xcd_grid(grid)),
+                       dim3(64 * PACK * (2 / NT)), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_attn<D, PACK, NT, false>), dim3(xcd_grid(grid)),
+                       dim3(64 * PACK * (2 / NT)), 0, s, a);
 }
 
 template <int D>
