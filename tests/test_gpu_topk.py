@@ -87,3 +87,35 @@ def test_topk_mask_feeds_the_pass():
     b = s.attn_fwd(qd, kd, vd, want_m, causal=True)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+def _tie_inputs(kind, B, Hq, Hkv, S_q, S_k, D):
+    q, k, _ = small_qkv(77, B, Hq, Hkv, S_q, S_k, D)
+    if kind == "equal":
+        # every row of Q and of K the same vector: every block mean, hence every
+        # score of a row, is the same number
+        q = q[:, :, :1].expand(-1, -1, S_q, -1).contiguous()
+        k = k[:, :, :1].expand(-1, -1, S_k, -1).contiguous()
+    else:
+        # Q = 0: every score is exactly zero (the products are signed zeros,
+        # and a sum that starts at +0 stays +0)
+        q = torch.zeros_like(q)
+    return q, k
+
+
+@pytest.mark.parametrize("kind", ["equal", "zero"])
+@pytest.mark.parametrize("causal", [True, False])
+def test_topk_mask_ties(kind, causal):
+    """All candidates of a row tie: the kept blocks are the smallest kb (the
+    oracle's order), on the radix path (rows of <= 512 key blocks) and on the
+    sorting path (longer rows)."""
+    s = steel()
+    dev = torch.device("cuda:0")
+    for S_k in (64 * 300 + 5, 64 * 700):
+        say(f"[topk] ties {kind}: causal={causal} S_k={S_k}")
+        q, k = _tie_inputs(kind, 1, 4, 2, 640, S_k, 64)
+        got = s.topk_block_mask(q.to(dev), k.to(dev), 1, 10, causal=causal)
+        torch.cuda.synchronize()
+        want = oracle.topk_meanpool_mask(q, k, 1, 10, causal)
+        got = got.cpu().numpy()
+        assert np.array_equal(got, want), f"{int((got != want).sum())} mask bytes differ"
