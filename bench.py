@@ -88,6 +88,24 @@ def traffic_for(workload):
     return entry.get("bytes_per_run")
 
 
+# Softmax work per element of a live tile, in VALU cycles of one SIMD for a
+# 64-lane instruction: exp2 (a transcendental, quarter rate: 16 cycles), the
+# fma that forms its argument (4), half a 3-input max (2), half a packed bf16
+# conversion (2), half a bf16 dot2 for the row sum (2): 26 cycles per 64
+# elements.
+VALU_CYCLES_PER_ELEM = (16 + 4 + 2 + 2 + 2) / 64.0
+
+
+def valu_bound(n_live, D):
+    """Time the softmax alone would take on all 1,024 SIMDs at 2.4 GHz: the
+    plain-ALU bound beside the MFMA one."""
+    cycles = n_live * 64 * 64 * VALU_CYCLES_PER_ELEM
+    us = cycles / (256 * 4 * 2.4e9) * 1e6
+    return {"bound": "alu", "us": round(us, 1),
+            "model": "per live element: exp2 (quarter rate) + fma + half max3 + half cvt_pk_bf16 + half dot2, 64 lanes per 4 cycles",
+            "mfma_us_at_peak": round(4.0 * 64 * 64 * D * n_live / PEAK_TFLOPS / 1e6, 1)}
+
+
 def blas_threads():
     try:
         from threadpoolctl import threadpool_info
@@ -247,6 +265,15 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
         step()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
+    # the same calls once more with an event between each two, for the median
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
+        step()
+        ev[i + 1].record()
+    torch.cuda.synchronize()
+    per_call = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    median_ms = per_call[steps // 2] if steps % 2 else 0.5 * (per_call[steps // 2 - 1] + per_call[steps // 2])
 
     # attention kernels alone: plan once, time runs with events on their stream
     plan = steel.Plan(md, cfg.B, cfg.Hq, cfg.Hkv, cfg.S_q, cfg.S_k, causal=cfg.causal, device=dev)
@@ -322,6 +349,8 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
         "pct_peak_dense": round(100 * f_dense / wall / 1e12 / PEAK_TFLOPS, 2),
         "peak_tflops": round(PEAK_TFLOPS, 1),
         "peak_basis": "256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU",
+        "ms_per_step_median": round(median_ms, 4),
+        "valu_bound": valu_bound(n_live, cfg.D),
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),
