@@ -116,9 +116,10 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 #define STEEL_XCD_GROUP 16
 #endif
 constexpr int kXcdGroup = STEEL_XCD_GROUP;
+template <int GROUP = kXcdGroup>
 __device__ __forceinline__ int xcd_slot(int b) {
   const int x = b & 7, j = b >> 3;
-  return ((j / kXcdGroup) * 8 + x) * kXcdGroup + j % kXcdGroup;
+  return ((j / GROUP) * 8 + x) * GROUP + j % GROUP;
 }
 inline int xcd_grid(int n) {
   const int m = 8 * kXcdGroup;

@@ -47,6 +47,14 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 constexpr int kW64Stages = 5;
+// GROUP: items of the work order dealt to each XCD in groups of this many
+// (see xcd_slot), chosen per launch.  With few items per workgroup, groups of
+// 4 spread the heavy end of the order over the XCDs more evenly (S = 4096
+// causal, 32/8 heads, 2 items per workgroup: 167 us and 283 MB read with
+// groups of 16, 151 us and 159 MB with 4).  With many, groups of 16 keep a
+// pack's neighbouring query blocks, which read mostly the same key/value
+// tiles, in one XCD's L2 (window/sink S = 16384, 8 items per workgroup: the
+// same time either way, 311 MB read with 16 and 471 MB with 4).
 
 // s_waitcnt vmcnt(n) for a count known at run time (n <= 2 tiles of copies);
 // larger values wait for everything.
@@ -110,8 +118,9 @@ __device__ __forceinline__ void mfma_acc(f32x16& acc, const bf16x8& a, const bf1
 // RAGGED: S_k is not a multiple of the block, so the last key block is cut
 // short and its copies clamp their rows.  Without it that path is compiled
 // out (its address arithmetic would otherwise run on every tile).
-template <int D, bool RAGGED>
+template <int D, bool RAGGED, int GROUP>
 __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
+  constexpr int kGroup = GROUP;
   constexpr int NW = 4;             // waves = query heads of the pack
   constexpr int C = D / 8;          // 16-byte chunks per row
   constexpr int TE = kBlk * D;      // bf16 elements per tile
@@ -176,8 +185,8 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   // items, but the lightest round first, so that workgroups whose items all
   // have the same length do not all reach their item boundaries (Q loads,
   // output stores) at the same moment.
-  const int n_x = (n_all / (8 * kXcdGroup)) * kXcdGroup +
-                  min(max(n_all % (8 * kXcdGroup) - kXcdGroup * xb, 0), kXcdGroup);
+  const int n_x = (n_all / (8 * kGroup)) * kGroup +
+                  min(max(n_all % (8 * kGroup) - kGroup * xb, 0), kGroup);
   const int K = (n_x + nwb - 1) / nwb;  // rounds of this XCD
   auto round_pos = [&](int k) __attribute__((always_inline)) -> int {  // -1: none
     if (k >= K) return -1;
@@ -194,7 +203,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   int w_item = -1, w_beg = 0, w_end = 0;
   auto load_items = [&](int win) __attribute__((always_inline)) {
     const int p = round_pos(64 * win + lane);
-    const int idx = p < 0 ? n_all : xcd_slot(8 * p + xb);
+    const int idx = p < 0 ? n_all : xcd_slot<kGroup>(8 * p + xb);
     w_item = -1;
     w_beg = 0;
     w_end = 0;
@@ -656,10 +665,16 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
 }
 
 hipError_t launch_attention_w64(const AttnArgs& a, hipStream_t s) {
-  if (a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn_w64<128, true>), dim3(256), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_attn_w64<128, false>), dim3(256), dim3(256), 0, s, a);
+  // the pack list has at most NP items (one per head pack and query block)
+  const long long np = (long long)a.R / 4;
+  const bool few = np <= 4ll * 256;
+  if (a.S_k % kBlk != 0) {
+    if (few) hipLaunchKernelGGL((k_attn_w64<128, true, 4>), dim3(256), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_w64<128, true, 16>), dim3(256), dim3(256), 0, s, a);
+  } else {
+    if (few) hipLaunchKernelGGL((k_attn_w64<128, false, 4>), dim3(256), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_w64<128, false, 16>), dim3(256), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
