@@ -28,11 +28,14 @@
  * surface at the caller's next synchronisation, as usual for HIP.
  *
  * Thread safety: calls may be made concurrently from several threads and on
- * several streams; the only process-wide state is one internal scratch
- * buffer per device and the thread-local error text.  Calls that use the
- * scratch buffer take turns while they enqueue (a short host lock) and are
- * ordered on the GPU by an event, so calls on different streams of one
- * device run one after the other.
+ * several streams.  The fused calls keep their index in a scratch buffer
+ * that belongs to the calling stream (one per device and stream, allocated on
+ * the stream's first call, grown when a call needs more, kept until the
+ * process ends): calls on one stream reuse it in stream order, and calls on
+ * different streams use different buffers, so they never wait for each
+ * other.  Two threads enqueueing on the same stream take turns while they
+ * enqueue (a short host lock per stream).  Besides these buffers the only
+ * process-wide state is the thread-local error text.
  */
 #ifndef STEEL_H
 #define STEEL_H
@@ -69,10 +72,11 @@ typedef enum steel_status {
  *
  * Inputs and output are owned by the caller; the library keeps no pointer to
  * them after it returns.  Internal workspace (the compressed live-block list
- * and the work order) lives in the device's scratch buffer, which the library
- * allocates on first use and grows (hipMalloc, synchronous) when a call needs
- * more than it holds; it is kept until the process ends.  Results are bitwise
- * reproducible run to run.
+ * and the work order) lives in the calling stream's scratch buffer, which the
+ * library allocates on the stream's first call and grows (hipMalloc,
+ * synchronous; the stream's earlier calls are waited for) when a call needs
+ * more than it holds; it is kept until the process ends.  Results are
+ * bitwise reproducible run to run.
  */
 int steel_attn_fwd(const void* q, const void* k, const void* v,
                    const uint8_t* block_mask, void* out,
@@ -122,10 +126,14 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
  *                               only reads it, so several runs may share one
  *                               plan concurrently
  *
- * run must be given the same B, Hq, Hkv, S_q, S_k, blk and causal as the plan
- * (the kernels check a header the plan writes and leave out untouched on a
- * mismatch), and must be ordered after the plan on the device (same stream,
- * or an event).  Arguments mean what they mean for steel_attn_fwd.
+ * run must be given the same B, Hq, Hkv, S_q, S_k, blk and causal as the plan:
+ * the plan writes a header with every one of them (and the head packing and
+ * causal limit derived from them) into the workspace, the attention kernels
+ * compare it with their own arguments, and on any mismatch they return
+ * without writing out (the call itself still returns STEEL_OK: the header is
+ * only readable on the device).  run must be ordered after the plan on the
+ * device (same stream, or an event).  Arguments mean what they mean for
+ * steel_attn_fwd.
  */
 size_t steel_attn_workspace_bytes(int B, int Hq, int Hkv, int S_q, int S_k, int blk);
 
@@ -239,9 +247,9 @@ int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, in
  *   keep_num, keep_den   1 <= keep_num <= keep_den (1 and 10: 10%)
  *   block_mask  uint8 device buffer of B*Hq*nQB*nKB bytes, caller-owned
  *
- * Float64 workspace for the block means and scores lives in the device's
- * scratch buffer (as for steel_attn_fwd); the call only enqueues, unless the
- * buffer must grow.  Errors as for steel_attn_fwd.
+ * Float64 workspace for the block means and scores lives in the calling
+ * stream's scratch buffer (as for steel_attn_fwd); the call only enqueues,
+ * unless the buffer must grow.  Errors as for steel_attn_fwd.
  */
 int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, int S_q,
                           int S_k, int D, int blk, int causal, int keep_num, int keep_den,

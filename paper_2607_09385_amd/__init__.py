@@ -45,6 +45,19 @@ def _check_bf16(name, t, ndim=4):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _check_out(out, shape, device):
+    """A caller-supplied fp32 output: the kernels write every element of a
+    contiguous [B, Hq, S_q, D] float32 buffer on q's device, nothing less."""
+    torch = _torch()
+    if not isinstance(out, torch.Tensor):
+        raise TypeError("out must be a torch.Tensor")
+    if out.dtype != torch.float32 or tuple(out.shape) != tuple(shape) or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous float32 tensor {list(shape)} "
+                         f"(got {out.dtype} {tuple(out.shape)})")
+    if out.device != device:
+        raise ValueError(f"out must be on q's device {device} (got {out.device})")
+
+
 def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal: bool = True,
              blk: int = BLK, out=None, stream=None):
     """Fused masked attention forward.
@@ -77,8 +90,7 @@ def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal:
     if out is None:
         out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
     else:
-        if out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
-            raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+        _check_out(out, (B, Hq, S_q, D), q.device)
     with torch.cuda.device(q.device):
         st = _lib.load().steel_attn_fwd(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(),
@@ -102,6 +114,8 @@ def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, cau
     Bk, Hkv, S_k, Dk = k.shape
     if tuple(v.shape) != tuple(k.shape) or Bk != B or Dk != D:
         raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    if q.device != k.device or q.device != v.device:
+        raise ValueError("q, k and v must be on the same device")
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     if causal_offset is None:
@@ -120,10 +134,12 @@ def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, cau
         out = torch.empty((B, Hq, S_q, D), dtype=odt, device=q.device)
     if lse is None:
         lse = torch.empty((B, Hq, S_q), dtype=torch.float32, device=q.device)
-    if out.dtype != odt or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
-        raise ValueError(f"out must be a contiguous {odt} tensor [B, Hq, S_q, D]")
-    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq, S_q) or not lse.is_contiguous():
-        raise ValueError("lse must be a contiguous float32 tensor [B, Hq, S_q]")
+    if out.dtype != odt or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous() \
+            or out.device != q.device:
+        raise ValueError(f"out must be a contiguous {odt} tensor [B, Hq, S_q, D] on q's device")
+    if lse.dtype != torch.float32 or tuple(lse.shape) != (B, Hq, S_q) or not lse.is_contiguous() \
+            or lse.device != q.device:
+        raise ValueError("lse must be a contiguous float32 tensor [B, Hq, S_q] on q's device")
     with torch.cuda.device(q.device):
         st = _lib.load().steel_attn_fwd_ex(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(), lse.data_ptr(),
@@ -176,8 +192,8 @@ def attn_fwd_window(q, k, v, window_blocks: int, sink_blocks: int = 0, *,
         scale = 1.0 / math.sqrt(D)
     if out is None:
         out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
-    elif out.dtype != torch.float32 or tuple(out.shape) != (B, Hq, S_q, D) or not out.is_contiguous():
-        raise ValueError("out must be a contiguous float32 tensor [B, Hq, S_q, D]")
+    else:
+        _check_out(out, (B, Hq, S_q, D), q.device)
     with torch.cuda.device(q.device):
         st = _lib.load().steel_attn_fwd_window(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, Hq, Hkv, S_q, S_k, D, blk,
@@ -285,10 +301,14 @@ class Plan:
         if tuple(q.shape) != (B, Hq, S_q, D) or tuple(k.shape) != (B, Hkv, S_k, D) \
                 or tuple(v.shape) != tuple(k.shape):
             raise ValueError("q, k, v do not match the planned shape")
+        if q.device != k.device or q.device != v.device or q.device != self.workspace.device:
+            raise ValueError("q, k, v and the plan's workspace must be on the same device")
         if scale is None:
             scale = 1.0 / math.sqrt(D)
         if out is None:
             out = torch.empty((B, Hq, S_q, D), dtype=torch.float32, device=q.device)
+        else:
+            _check_out(out, (B, Hq, S_q, D), q.device)
         with torch.cuda.device(q.device):
             st = _lib.load().steel_attn_run(
                 q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), B, Hq, Hkv, S_q, S_k,

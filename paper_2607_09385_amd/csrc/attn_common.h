@@ -30,9 +30,21 @@ struct AttnArgs {
   const int32_t* order;
   const int32_t* n_items;   // this list's item count
   const int32_t* header;    // plan header (after the two counts)
-  int Hq, Hkv, S_q, S_k, nQB, nKB, G, causal, delta, R, pack;
+  int B, Hq, Hkv, S_q, S_k, nQB, nKB, G, causal, delta, R, pack;
   float c;  // scale * log2(e)
 };
+
+typedef const __attribute__((address_space(4))) int32_t* cint_p;
+
+// The plan header (written by the index build) describes the same problem as
+// the kernel's arguments: every size, the causal limit and the head packing.
+__device__ __forceinline__ bool plan_matches(const AttnArgs& a) {
+  const cint_p h = (cint_p)a.header;
+  return h[kPfMagic] == kPlanMagic && h[kPfR] == a.R && h[kPfNKB] == a.nKB &&
+         h[kPfPack] == a.pack && h[kPfCausal] == a.causal && h[kPfDelta] == a.delta &&
+         h[kPfB] == a.B && h[kPfHq] == a.Hq && h[kPfHkv] == a.Hkv && h[kPfSq] == a.S_q &&
+         h[kPfSk] == a.S_k;
+}
 
 __device__ __forceinline__ float other_half_max(float x) {
   const unsigned u = __float_as_uint(x);
@@ -126,7 +138,6 @@ inline int xcd_grid(int n) {
   return (n + m - 1) / m * m;
 }
 
-typedef const __attribute__((address_space(4))) int32_t* cint_p;
 typedef const __attribute__((address_space(4))) uint32_t* cuint_p;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 

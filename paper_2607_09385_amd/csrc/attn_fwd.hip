@@ -82,10 +82,7 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
 
   // index data is read-only during the kernel: scalar loads
-  const cint_p hd = (cint_p)a.header;
-  if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
-      hd[4] != a.causal || hd[5] != a.delta)
-    return;  // index was planned for another problem: leave out untouched
+  if (!plan_matches(a)) return;  // index planned for another problem: out untouched
   const int idx = xcd_slot((int)blockIdx.x);
   if (idx >= ((cint_p)a.n_items)[0]) return;
   const int item = ((cint_p)a.order)[idx];
@@ -469,8 +466,9 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.col = w.col;
   a.order = nullptr;
   a.n_items = nullptr;
-  a.header = w.n_items + 2;
+  a.header = w.n_items + kPlanAt;
   a.nKB = p.nKB;
+  a.B = p.B;
   a.R = p.R;
   a.pack = p.pack;
   a.Hq = p.Hq;

@@ -135,10 +135,7 @@ __global__ __launch_bounds__(256, 1) void k_attn_w64(AttnArgs a) {
   static_assert(2 * KS * 2 == 32 && 4 * DT * 2 == 32, "32 slots of one QK and one PV MFMA");
   __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
 
-  const cint_p hd = (cint_p)a.header;
-  if (hd[0] != kPlanMagic || hd[1] != a.R || hd[2] != a.nKB || hd[3] != a.pack ||
-      hd[4] != a.causal || hd[5] != a.delta)
-    return;  // index was planned for another problem: leave out untouched
+  if (!plan_matches(a)) return;  // index planned for another problem: out untouched
   const int n_all = ((cint_p)a.n_items)[0];
 
   const int tid = threadIdx.x, lane = tid & 63;

@@ -161,12 +161,18 @@ __device__ int wg_scan_array(int* a, long long n, int* sh) {
 }
 
 __device__ __forceinline__ void write_header(const Problem& p, int32_t* n_items) {
-  n_items[2] = kPlanMagic;
-  n_items[3] = p.R;
-  n_items[4] = p.nKB;
-  n_items[5] = p.pack;
-  n_items[6] = p.causal;
-  n_items[7] = p.delta;
+  int32_t* h = n_items + kPlanAt;
+  h[kPfMagic] = kPlanMagic;
+  h[kPfR] = p.R;
+  h[kPfNKB] = p.nKB;
+  h[kPfPack] = p.pack;
+  h[kPfCausal] = p.causal;
+  h[kPfDelta] = p.delta;
+  h[kPfB] = p.B;
+  h[kPfHq] = p.Hq;
+  h[kPfHkv] = p.Hkv;
+  h[kPfSq] = p.S_q;
+  h[kPfSk] = p.S_k;
 }
 
 // Histogram index of (bin, chunk): bins descending from the list's top bin,

@@ -54,14 +54,21 @@ struct IndexBuffers {
   int32_t* order_s;    // [R]   single-head items, heaviest first
   int32_t* order_p;    // [NP]  head-pack items, heaviest first
   int32_t* n_items;    // [kHeaderInts] {single items, pack items, plan header,
-                       //   top bins of the two lists}
+                       //   top bins of the two lists} (see kPlanAt, kTopBin)
 };
 
 // Plan header written after the two item counts; the attention kernels check
-// it against their own arguments before touching the index.
+// it against their own arguments before touching the index, so a run with
+// other sizes, another causal limit or another head packing than the plan
+// leaves its output untouched.  Layout of n_items: [0] single-head items,
+// [1] head-pack items, [kPlanAt + f] field f of PlanField, [kTopBin + list]
+// the top work-order bin of each list.
 constexpr int kPlanMagic = 0x5354454c;  // "STEL"
-constexpr int kTopBin = 8;
-constexpr int kHeaderInts = 10;
+enum PlanField { kPfMagic, kPfR, kPfNKB, kPfPack, kPfCausal, kPfDelta, kPfB, kPfHq, kPfHkv,
+                 kPfSq, kPfSk, kPlanFields };
+constexpr int kPlanAt = 2;
+constexpr int kTopBin = kPlanAt + kPlanFields;
+constexpr int kHeaderInts = kTopBin + 2;
 
 __host__ __device__ inline int nchunks(int n) { return (n + kChunk - 1) / kChunk; }
 

@@ -1,18 +1,22 @@
 // C ABI of libsteel: argument checks, workspace, launches.
 //
 // Every check runs before the first HIP call, so an invalid call enqueues
-// nothing and writes no output.  Workspace for the live-block index comes
-// from a per-device stream-ordered memory pool (kept across calls, never
-// trimmed), so a call stays asynchronous and may overlap calls on other
-// streams.
+// nothing and writes no output.  The fused calls keep the live-block index in
+// a scratch buffer owned by the calling stream (one per device and stream,
+// kept for the life of the process): calls on one stream reuse it in stream
+// order, calls on different streams never share it, so a call only enqueues
+// and calls on different streams overlap.  The two-phase plan/run form takes
+// caller-owned workspace instead.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <memory>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/steel.h"
 #include "internal.h"
@@ -39,23 +43,41 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 constexpr int kMaxDevices = 64;
 
-// Internal scratch (the live-block index of a fused call, the means and
-// scores of the mask producer): one buffer per device, kept for the life of
-// the process and grown when a call needs more.  A stream-ordered pool
-// allocation per call made every call wait on the host for the previous one
-// (the runtime waits for the block's release), so calls could not be queued
-// ahead.  Reuse is ordered on the GPU instead: each call makes its stream wait
-// for the completion event of the previous user of the buffer and records its
-// own; host threads take turns while they enqueue (the lock is held from
-// scratch_begin to scratch_end).
-struct DeviceScratch {
+// Scratch of the fused calls (the live-block index; the means and scores of
+// the mask producer): one buffer per (device, stream), kept for the life of
+// the process and grown when a call needs more.  Work on one stream runs in
+// issue order, so a stream's buffer is reused without any wait; buffers of
+// different streams are distinct, so calls on different streams never wait
+// for each other.  A slot's lock is held from scratch_begin to scratch_end,
+// so two host threads enqueueing on the same stream do not interleave their
+// kernels over one buffer.  Each use records an event that the next use of
+// the slot waits for on its stream: that keeps the order if a stream is
+// destroyed and a new one gets the same handle.  A (stream-ordered) pool
+// allocation per call was not used: it made every call wait on the host for
+// the previous one's release.
+struct StreamScratch {
+  hipStream_t stream = nullptr;
   std::mutex mu;
   char* ptr = nullptr;
   size_t bytes = 0;
   hipEvent_t done = nullptr;  // completion of the last call that used ptr
   bool recorded = false;
 };
+struct DeviceScratch {
+  std::mutex mu;  // guards the list (slots are never removed)
+  std::vector<std::unique_ptr<StreamScratch>> slots;
+};
 DeviceScratch g_scratch[kMaxDevices];
+
+StreamScratch* stream_slot(int dev, hipStream_t s) {
+  DeviceScratch& d = g_scratch[dev];
+  std::lock_guard<std::mutex> g(d.mu);
+  for (auto& sl : d.slots)
+    if (sl->stream == s) return sl.get();
+  d.slots.emplace_back(new StreamScratch);
+  d.slots.back()->stream = s;
+  return d.slots.back().get();
+}
 
 // Selects dev for the calls in its scope and restores the caller's device.
 struct DeviceScope {
@@ -71,9 +93,10 @@ struct DeviceScope {
 };
 
 int scratch_begin(int dev, hipStream_t s, size_t need, std::unique_lock<std::mutex>* lk,
-                  char** out) {
-  DeviceScratch& d = g_scratch[dev];
+                  StreamScratch** slot, char** out) {
+  StreamScratch& d = *stream_slot(dev, s);
   *lk = std::unique_lock<std::mutex>(d.mu);
+  *slot = &d;
   DeviceScope scope(dev);
   if (scope.err != hipSuccess) return hip_fail(scope.err, "selecting the stream's device");
   hipError_t e = hipSuccess;
@@ -81,6 +104,7 @@ int scratch_begin(int dev, hipStream_t s, size_t need, std::unique_lock<std::mut
     return hip_fail(e, "creating the scratch event");
   if (need > d.bytes) {
     if (d.ptr) {
+      // only this stream's earlier calls can still read the old buffer
       if (d.recorded && (e = hipEventSynchronize(d.done)) != hipSuccess)
         return hip_fail(e, "waiting for the previous user of the scratch buffer");
       if ((e = hipFree(d.ptr)) != hipSuccess) return hip_fail(e, "releasing the scratch buffer");
@@ -101,17 +125,16 @@ int scratch_begin(int dev, hipStream_t s, size_t need, std::unique_lock<std::mut
   return STEEL_OK;
 }
 
-// After the call's work is enqueued on s (lock still held).
-int scratch_end(int dev, hipStream_t s) {
-  DeviceScratch& d = g_scratch[dev];
+// After the call's work is enqueued on s (slot lock still held).
+int scratch_end(StreamScratch* slot, int dev, hipStream_t s) {
   DeviceScope scope(dev);
   if (scope.err != hipSuccess) return hip_fail(scope.err, "selecting the stream's device");
-  hipError_t e = hipEventRecord(d.done, s);
+  hipError_t e = hipEventRecord(slot->done, s);
   if (e != hipSuccess) {
-    d.recorded = false;
+    slot->recorded = false;
     return hip_fail(e, "recording the scratch buffer's use");
   }
-  d.recorded = true;
+  slot->recorded = true;
   return STEEL_OK;
 }
 
@@ -256,13 +279,14 @@ int fused_call(const steel::Problem& p, const void* q, const void* k, const void
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
   const Layout L = layout(p, true);
   std::unique_lock<std::mutex> lk;
+  StreamScratch* slot = nullptr;
   char* ws = nullptr;
-  if ((rc = scratch_begin(dev, s, L.total, &lk, &ws)) != STEEL_OK) return rc;
+  if ((rc = scratch_begin(dev, s, L.total, &lk, &slot, &ws)) != STEEL_OK) return rc;
   const steel::IndexBuffers w = carve(ws, L);
   hipError_t e = steel::launch_block_index(p, block_mask, w, s);
   if (e == hipSuccess)
     e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), lse, scale, w, s);
-  const int re = scratch_end(dev, s);
+  const int re = scratch_end(slot, dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   return re;
 }
@@ -425,13 +449,14 @@ int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, 
   const size_t o_km = align256(n_qm * sizeof(double)), o_sc = o_km + align256(n_km * sizeof(double));
   const size_t total = o_sc + align256(n_sc * sizeof(double));
   std::unique_lock<std::mutex> lk;
+  StreamScratch* slot = nullptr;
   char* ws = nullptr;
-  if ((rc = scratch_begin(dev, s, total, &lk, &ws)) != STEEL_OK) return rc;
+  if ((rc = scratch_begin(dev, s, total, &lk, &slot, &ws)) != STEEL_OK) return rc;
   hipError_t e = steel::launch_topk_mask(
       p, static_cast<const __bf16*>(q), static_cast<const __bf16*>(k), keep_num, keep_den,
       block_mask, reinterpret_cast<double*>(ws), reinterpret_cast<double*>(ws + o_km),
       reinterpret_cast<double*>(ws + o_sc), s);
-  const int re = scratch_end(dev, s);
+  const int re = scratch_end(slot, dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   return re;
 }
@@ -451,8 +476,9 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
   const Layout L = layout(p, false);
   std::unique_lock<std::mutex> lk;
+  StreamScratch* slot = nullptr;
   char* ws = nullptr;
-  if ((rc = scratch_begin(dev, s, L.total, &lk, &ws)) != STEEL_OK) return rc;
+  if ((rc = scratch_begin(dev, s, L.total, &lk, &slot, &ws)) != STEEL_OK) return rc;
   steel::IndexBuffers w;
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
@@ -463,7 +489,7 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   w.col = col;
   w.order_s = order;
   hipError_t e = steel::launch_block_index(p, block_mask, w, s);
-  const int re = scratch_end(dev, s);
+  const int re = scratch_end(slot, dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   return re;
 }

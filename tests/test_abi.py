@@ -5,6 +5,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2607_09385_amd as steel
@@ -184,3 +185,22 @@ def test_lse_and_merge_entry_points_reject_invalid():
     assert st == 1 and "non-NULL" in _lib.last_error()
     st = lib.steel_attn_merge(FAKE + 4, FAKE, 2, 10, 64, FAKE, None, None)
     assert st == 1 and "aligned" in _lib.last_error()
+
+
+def test_output_buffer_validation():
+    """The binding's check of caller-supplied fp32 outputs (used by attn_fwd,
+    attn_fwd_window and Plan.run) runs on the host."""
+    torch = pytest.importorskip("torch")
+    from paper_2607_09385_amd import _check_out
+    dev = torch.device("cpu")
+    _check_out(torch.empty((1, 2, 64, 64)), (1, 2, 64, 64), dev)
+    with pytest.raises(ValueError, match="contiguous float32"):
+        _check_out(torch.empty((1, 2, 63, 64)), (1, 2, 64, 64), dev)
+    with pytest.raises(ValueError, match="contiguous float32"):
+        _check_out(torch.empty((1, 2, 64, 64), dtype=torch.bfloat16), (1, 2, 64, 64), dev)
+    with pytest.raises(ValueError, match="contiguous float32"):
+        _check_out(torch.empty((1, 2, 64, 64)).transpose(2, 3), (1, 2, 64, 64), dev)
+    with pytest.raises(ValueError, match="device"):
+        _check_out(torch.empty((1, 2, 64, 64)), (1, 2, 64, 64), torch.device("cuda", 0))
+    with pytest.raises(TypeError):
+        _check_out(np.zeros((1, 2, 64, 64), dtype=np.float32), (1, 2, 64, 64), dev)

@@ -38,11 +38,14 @@ def steel():
 
 
 def run(q, k, v, m, scale, causal, stream=None):
+    """One fused call; the output buffer starts as NaN, so an element the
+    kernels skip (a work item lost or a row never stored) cannot pass."""
     s = steel()
     dev = torch.device("cuda:0")
     qd, kd, vd = q.to(dev), k.to(dev), v.to(dev)
     md = None if m is None else torch.from_numpy(np.ascontiguousarray(m)).to(dev)
-    out = s.attn_fwd(qd, kd, vd, md, scale=scale, causal=causal, stream=stream)
+    out = torch.full(tuple(q.shape), float("nan"), dtype=torch.float32, device=dev)
+    s.attn_fwd(qd, kd, vd, md, scale=scale, causal=causal, stream=stream, out=out)
     torch.cuda.synchronize()
     return out.cpu().numpy().astype(np.float64)
 

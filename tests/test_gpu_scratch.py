@@ -1,12 +1,13 @@
-"""Calls that share the library's per-device scratch buffer (the live-block
-index of a fused call, the float64 workspace of the mask producer) from
-several streams and several host threads.
+"""Fused calls from several streams and several host threads.  Each stream
+keeps its own scratch buffer for the live-block index (the float64 workspace
+of the mask producer lives there too); calls on one stream reuse it in
+stream order, and two threads enqueueing on one stream take turns.
 
 Each call's result must equal, bit for bit, the result of the same call made
 alone on one stream (the library's results are reproducible run to run), and
 one case is anchored to the float64 oracle.  A call whose index needs more
-scratch than any earlier call makes the buffer grow between queued calls on
-two streams.
+scratch than any earlier call on its stream makes that stream's buffer grow
+while calls are queued on both streams.
 """
 import math
 import sys
@@ -69,7 +70,7 @@ def call(s, name, inputs, kw, stream):
     return out
 
 
-def test_fused_calls_on_two_streams_share_scratch():
+def test_fused_calls_on_two_streams():
     s = steel()
     dev = torch.device("cuda:0")
     data = {n: make(n, dev) for n in CASES}
@@ -138,5 +139,41 @@ def test_fused_calls_from_two_threads():
     assert not errors, errors
     for t in range(2):
         assert len(results[t]) == 6
+        for n, o in results[t]:
+            assert torch.equal(o, ref[n]), f"thread {t}: {n} differs from the one-stream result"
+
+
+def test_two_threads_on_one_stream():
+    """Both threads enqueue on the same stream and so reuse one scratch
+    buffer: the per-stream lock keeps each call's index build and attention
+    pass together."""
+    s = steel()
+    dev = torch.device("cuda:0")
+    names = ["packs_masked", "mha_d64", "noncausal_gqa"]
+    data = {n: make(n, dev) for n in names}
+    ref = {n: call(s, n, data[n][1], data[n][2], torch.cuda.current_stream()) for n in names}
+    torch.cuda.synchronize()
+    shared = torch.cuda.Stream()
+    results = {0: [], 1: []}
+    errors = []
+
+    def worker(t):
+        try:
+            for r in range(8):
+                n = names[(r + t) % 3]
+                results[t].append((n, call(s, n, data[n][1], data[n][2], shared)))
+        except Exception as e:  # reported in the main thread
+            errors.append(repr(e))
+
+    say("[scratch] two host threads, one shared stream")
+    th = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    shared.synchronize()
+    assert not errors, errors
+    for t in range(2):
+        assert len(results[t]) == 8
         for n, o in results[t]:
             assert torch.equal(o, ref[n]), f"thread {t}: {n} differs from the one-stream result"
