@@ -35,7 +35,8 @@
  * different streams use different buffers, so they never wait for each
  * other.  Two threads enqueueing on the same stream take turns while they
  * enqueue (a short host lock per stream).  Besides these buffers the only
- * process-wide state is the thread-local error text.
+ * process-wide state is the thread-local error text and the fixed array of
+ * steel_attn_fwd_noalloc.
  */
 #ifndef STEEL_H
 #define STEEL_H
@@ -254,6 +255,38 @@ int steel_attn_plan_window(int B, int Hq, int Hkv, int S_q, int S_k, int blk, in
 int steel_topk_block_mask(const void* q, const void* k, int B, int Hq, int Hkv, int S_q,
                           int S_k, int D, int blk, int causal, int keep_num, int keep_den,
                           uint8_t* block_mask, void* stream);
+
+/*
+ * steel_attn_fwd for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same computation, arguments, checks and kernels, bitwise the same
+ * output, but the live-block index is built in a fixed array of
+ * STEEL_NOALLOC_SCRATCH_BYTES that the library holds on each device it runs on
+ * (a file-scope device array, present from the library's load until the
+ * process ends).  The call allocates nothing: no hipMalloc, hipFree or
+ * allocating library routine.  The first call on a device looks up that
+ * device's copy of the array (hipGetSymbolAddress); later calls only enqueue.
+ *
+ *   Limit: the index of the problem must fit the array.  It needs about
+ *   4 * R * (nKB + 4) bytes plus 2 KiB per 256 rows (R = B*Hq*ceil(S_q/64),
+ *   nKB = ceil(S_k/64)): 24.3 MiB for 24 heads at S = 32768, 8.2 MiB for
+ *   32 heads at S = 16384 (steel_attn_workspace_bytes gives the exact
+ *   figure).  A larger problem returns STEEL_ERR_UNSUPPORTED before any HIP
+ *   call (use steel_attn_fwd or plan/run).
+ *
+ *   Every call on one device shares that device's array, which keeps the last
+ *   call's index: calls that overlap on one device (concurrent streams, or
+ *   threads enqueueing on different streams) race on it and must be ordered
+ *   by the caller; calls queued on one stream are ordered by the stream.
+ *   Nothing in the array needs to start at zero (each call writes all it
+ *   reads).
+ */
+#define STEEL_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+int steel_attn_fwd_noalloc(const void* q, const void* k, const void* v,
+                           const uint8_t* block_mask, void* out,
+                           int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
+                           float scale, int causal, void* stream);
 
 /* Text of the last non-OK status returned on the calling thread ("" if none). */
 const char* steel_last_error(void);

@@ -63,6 +63,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_attn_fwd_ex.restype = c_int
     lib.steel_attn_fwd_ex.argtypes = [c_void_p] * 6 + [c_int] * 7 + [c_float, c_int, c_int, c_int,
                                                                      c_void_p]
+    lib.steel_attn_fwd_noalloc.restype = c_int
+    lib.steel_attn_fwd_noalloc.argtypes = list(lib.steel_attn_fwd.argtypes)
     lib.steel_attn_merge.restype = c_int
     lib.steel_attn_merge.argtypes = [c_void_p, c_void_p, c_int, ctypes.c_longlong, c_int, c_void_p,
                                      c_void_p, c_void_p]

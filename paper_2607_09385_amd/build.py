@@ -19,7 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsteel.so")
 SOURCES = ["steel_api.cpp", "block_index.hip", "block_select.hip", "attn_fwd.hip", "attn_w64.hip",
-           "attn_merge.hip"]
+           "attn_merge.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of every code object: the compiler would

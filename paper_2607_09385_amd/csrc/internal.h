@@ -80,6 +80,15 @@ constexpr uint32_t kUniformBit = 1u << 30;
 // histograms in LDS (4 + 4 * kBins / kChunk = 12 bytes per row: 144 KiB).
 constexpr int kFastRows = 12288;
 
+// Size of the fixed per-device scratch array of steel_attn_fwd_noalloc (the
+// live-block index of one call: counts, histograms, row_ptr, the list
+// capacity R * nKB and the work orders).  Equals STEEL_NOALLOC_SCRATCH_BYTES.
+constexpr size_t kNoAllocBytes = (size_t)32 << 20;
+
+// Device address of this device's copy of that array (looked up on the
+// first call for a device, with the device made current, then cached).
+hipError_t noalloc_scratch(int dev, char** ptr);
+
 // Enqueue the index build.  With p.pack == 1 every row is a single-head item.
 hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const IndexBuffers& w,
                               hipStream_t stream);

@@ -6,7 +6,8 @@
 // kept for the life of the process): calls on one stream reuse it in stream
 // order, calls on different streams never share it, so a call only enqueues
 // and calls on different streams overlap.  The two-phase plan/run form takes
-// caller-owned workspace instead.
+// caller-owned workspace instead, and steel_attn_fwd_noalloc a fixed
+// per-device array (noalloc.hip) that no call allocates.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -343,6 +344,35 @@ int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t
   set_pack(&p);
   p.heads_share_mask = block_mask == nullptr;
   return fused_call(p, q, k, v, block_mask, out, lse, scale, stream);
+}
+
+int steel_attn_fwd_noalloc(const void* q, const void* k, const void* v,
+                           const uint8_t* block_mask, void* out, int B, int Hq, int Hkv, int S_q,
+                           int S_k, int D, int blk, float scale, int causal, void* stream) {
+  g_err.clear();
+  steel::Problem p{};
+  int rc = check_attn(q, k, v, out, B, Hq, Hkv, S_q, S_k, D, blk, scale, causal, &p);
+  if (rc != STEEL_OK) return rc;
+  set_pack(&p);
+  p.heads_share_mask = block_mask == nullptr;
+  const Layout L = layout(p, true);
+  if (L.total > steel::kNoAllocBytes)
+    return fail(STEEL_ERR_UNSUPPORTED,
+                "the index of this problem needs %zu bytes of scratch; steel_attn_fwd_noalloc "
+                "holds %zu (use steel_attn_fwd or plan/run)",
+                L.total, steel::kNoAllocBytes);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = 0;
+  if ((rc = stream_device(s, &dev)) != STEEL_OK) return rc;
+  char* ws = nullptr;
+  hipError_t e = steel::noalloc_scratch(dev, &ws);
+  if (e != hipSuccess) return hip_fail(e, "looking up the fixed scratch array");
+  const steel::IndexBuffers w = carve(ws, L);
+  e = steel::launch_block_index(p, block_mask, w, s);
+  if (e == hipSuccess)
+    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), nullptr, scale, w, s);
+  if (e != hipSuccess) return hip_fail(e, "launching kernels");
+  return STEEL_OK;
 }
 
 int steel_attn_merge(const float* o_parts, const float* lse_parts, int n_parts, long long rows,

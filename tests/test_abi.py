@@ -204,3 +204,18 @@ def test_output_buffer_validation():
         _check_out(torch.empty((1, 2, 64, 64)), (1, 2, 64, 64), torch.device("cuda", 0))
     with pytest.raises(TypeError):
         _check_out(np.zeros((1, 2, 64, 64), dtype=np.float32), (1, 2, 64, 64), dev)
+
+
+def test_noalloc_rejects_oversized_index_before_any_hip_call():
+    lib = _lib.load()
+    # 32 heads at S = 65536: the index needs 64 MiB, the fixed array holds 32
+    st = lib.steel_attn_fwd_noalloc(FAKE, FAKE, FAKE, None, FAKE, 1, 32, 8, 65536, 65536, 64, 64,
+                                    0.125, 1, None)
+    assert st == 2 and "noalloc" in _lib.last_error()
+    need = lib.steel_attn_workspace_bytes(1, 32, 8, 65536, 65536, 64)
+    assert need > 32 << 20
+    # the largest named index fits
+    assert lib.steel_attn_workspace_bytes(1, 24, 24, 32768, 32768, 64) <= 32 << 20
+    st = lib.steel_attn_fwd_noalloc(FAKE, FAKE, FAKE, None, FAKE, 1, 4, 2, 128, 128, 96, 64,
+                                    0.125, 1, None)
+    assert st == 2 and "D=96" in _lib.last_error()
