@@ -47,7 +47,7 @@ PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12     # 2516.6
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_09385_amd", "csrc", f)
-               for f in ("attn_common.h", "attn_fwd.hip", "attn_w64.hip")]
+               for f in ("attn_common.h", "attn_fwd.hip", "attn_ws.hip")]
 
 
 def live_tile_counts(mask, B, Hq, S_q, S_k, causal, blk=64):
@@ -117,6 +117,18 @@ def blas_threads():
     return len(os.sched_getaffinity(0))
 
 
+def cpu_model():
+    """The host CPU's model name, from /proc/cpuinfo."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(cfg, q, k, v, mask, counts, seconds):
     """Time the float64 oracle on groups of 16 whole query blocks, cycling over
     heads, until ``seconds`` have passed; report live TFLOP/s of what it
@@ -144,11 +156,58 @@ def cpu_baseline(cfg, q, k, v, mask, counts, seconds):
         "value": live_flops / el / 1e12,
         "unit": "TFLOP/s",
         "cores": blas_threads(),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": (f"{done_rows} query rows ({n_groups} groups of 16 query blocks of one head, "
                    f"random order) of the same workload, float64, full score rows; {el:.1f} s"),
         "seconds": el,
     }
+
+
+def mfma_peak(iters=400000, waves_per_wg=4):
+    """Achievable rate of v_mfma_f32_32x32x16_bf16 (the instruction of both
+    attention products) on this chip, for constant and for N(0,1) operands:
+    the chip lowers its clock under the matrix cores' data-dependent power
+    draw, so this is the context for the roofline fraction, whose
+    denominator stays the published peak.  One workgroup of waves_per_wg
+    waves per CU; the average clock comes from the kernel's own counters
+    (shader cycles over 100 MHz reference ticks)."""
+    import torch
+    from paper_2607_09385_amd import _lib
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    grid = 256
+    sink = torch.empty(grid * 64 * waves_per_wg, dtype=torch.float32, device=dev)
+    clocks = torch.zeros(2 * grid, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    g = torch.Generator().manual_seed(0)
+    res = {"instruction": "v_mfma_f32_32x32x16_bf16", "grid": grid, "waves_per_cu": waves_per_wg,
+           "iters": iters}
+    for kind in ("constant", "normal"):
+        if kind == "constant":
+            ops = torch.ones((8, 64, 8), dtype=torch.bfloat16)
+        else:
+            ops = torch.randn((8, 64, 8), generator=g).to(torch.bfloat16)
+        ops = ops.to(dev)
+
+        def launch(n):
+            st = lib.steel_mfma_peak(ops.data_ptr(), n, grid, waves_per_wg, sink.data_ptr(),
+                                     clocks.data_ptr(), stream.cuda_stream)
+            if st != 0:
+                raise RuntimeError(f"steel_mfma_peak failed ({st})")
+        launch(iters // 4)   # clock ramp
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        launch(iters)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / 1e3
+        flops = grid * waves_per_wg * iters * 16 * 2.0 * 32 * 32 * 16
+        c = clocks.view(grid, 2).cpu().double()
+        ghz = float((c[:, 0] / (c[:, 1] / 100e6)).mean() / 1e9)
+        res[kind] = {"tflops": round(flops / t / 1e12, 1), "frac_of_peak": round(flops / t / 1e12 / PEAK_TFLOPS, 3),
+                     "ms": round(t * 1e3, 2), "avg_clock_ghz": round(ghz, 3)}
+    return res
 
 
 COPY_BYTES = 256 << 20   # reference elementwise kernel for the counter scale
@@ -358,7 +417,7 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_TFLOPS, 4),
             "traffic": traffic,
-            "kernel": "attention run (k_attn_w64 for uniform head packs of 4 at D=128, k_attn for the other items), index prebuilt",
+            "kernel": "attention run (k_attn_ws for uniform head packs of 4 at D=128, k_attn for the other items), index prebuilt",
             "run_us": round(run_s * 1e6, 2),
             "algorithmic_flops_per_run": f_live,
         },
@@ -400,7 +459,7 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
 
 
 def unfused_attention(qd, kd, vd, hidden, scale):
-    """Layer-by-layer attention on the same GPU (the comparison of Section V-C:
+    """Layer-by-layer attention on the same GPU (the comparison of Section V-B:
     every stage writes its result to HBM and the next reads it back):
     S = scale * Q K^T (hipBLASLt bf16 GEMM, materialised), masked with -inf,
     P = softmax(S) (materialised, bf16), O = P V (hipBLASLt).  ``hidden`` is the
@@ -588,6 +647,8 @@ def main():
                     help="layer-by-layer baseline against the fused call (one JSON line)")
     ap.add_argument("--merge", type=int, default=0, metavar="PARTS",
                     help="time steel_attn_merge over PARTS partial outputs of the workload's shape")
+    ap.add_argument("--mfma-peak", action="store_true",
+                    help="achievable bf16 MFMA rate for constant and N(0,1) operands (one JSON line)")
     ap.add_argument("--unfused-traffic-run", action="store_true",
                     help="workload for counter passes over the layer-by-layer baseline")
     ap.add_argument("--unfused-traffic-from", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -607,6 +668,9 @@ def main():
         sys.exit(2)
     if args.traffic_run:
         traffic_run(args.workload, args.steps if args.steps != 50 else 5)
+        return
+    if args.mfma_peak:
+        print(json.dumps({"mfma_peak": mfma_peak(), "peak_tflops": round(PEAK_TFLOPS, 1)}), flush=True)
         return
     if args.merge:
         print(json.dumps(bench_merge(args.workload, args.merge, args.steps, args.warmup)), flush=True)

@@ -68,6 +68,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_attn_merge.restype = c_int
     lib.steel_attn_merge.argtypes = [c_void_p, c_void_p, c_int, ctypes.c_longlong, c_int, c_void_p,
                                      c_void_p, c_void_p]
+    lib.steel_mfma_peak.restype = c_int
+    lib.steel_mfma_peak.argtypes = [c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

@@ -18,8 +18,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsteel.so")
-SOURCES = ["steel_api.cpp", "block_index.hip", "block_select.hip", "attn_fwd.hip", "attn_w64.hip",
-           "attn_merge.hip", "noalloc.hip"]
+SOURCES = ["steel_api.cpp", "block_index.hip", "block_select.hip", "attn_fwd.hip", "attn_ws.hip",
+           "attn_merge.hip", "noalloc.hip", "mfma_peak.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of every code object: the compiler would
@@ -30,11 +30,11 @@ COMMON = [
     "-Wno-unused-command-line-argument",
 ]
 # Both attention sources keep the compiler's MFMA accumulators in VGPRs: the
-# softmax reads the scores with VALU instructions, and AGPR-resident scores
-# would cost a copy per element.  (attn_w64.hip places its output
-# accumulator in AGPRs itself.)
+# softmax reads the scores with VALU instructions (AGPR-resident scores would
+# cost a copy per element), and attn_ws.hip runs two waves per SIMD, whose
+# 256 registers each hold no AGPR file.
 PER_SOURCE = {"attn_fwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
-              "attn_w64.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+              "attn_ws.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
 
 
 def hipcc() -> str:

@@ -124,10 +124,7 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
 // query blocks, mostly the same key/value tiles) then share one XCD's L2,
 // while every XCD still works from the heavy end of the order first.  The
 // grid is a multiple of 8 * kXcdGroup; positions past the item count exit.
-#ifndef STEEL_XCD_GROUP
-#define STEEL_XCD_GROUP 16
-#endif
-constexpr int kXcdGroup = STEEL_XCD_GROUP;
+constexpr int kXcdGroup = 16;
 template <int GROUP = kXcdGroup>
 __device__ __forceinline__ int xcd_slot(int b) {
   const int x = b & 7, j = b >> 3;
@@ -143,8 +140,9 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 template <int P> struct Par { static constexpr int value = P; };
 
-// Head packs of 4 at D = 128: one wave per head, persistent (attn_w64.hip).
-hipError_t launch_attention_w64(const AttnArgs& a, hipStream_t s);
+// Head packs of 4 at D = 128: two waves per head (scores and softmax; P V and
+// output), persistent (attn_ws.hip).
+hipError_t launch_attention_ws(const AttnArgs& a, hipStream_t s);
 
 
 }  // namespace steel

@@ -31,41 +31,22 @@
 
 #include "attn_common.h"
 
-#ifndef STEEL_NT
-#define STEEL_NT 1
-#endif
-#ifndef STEEL_STAGES_SINGLE
-#define STEEL_STAGES_SINGLE 2
-#endif
-#ifndef STEEL_STAGES
-#define STEEL_STAGES 4
-#endif
-#ifndef STEEL_W64
-#define STEEL_W64 1
-#endif
-
 namespace steel {
 
 // Depth of the K/V ring (stages of one K tile and one V tile each).  A
 // single-head workgroup has only two waves, so it keeps the ring short and
 // leaves LDS for more workgroups per CU.
-template <int D, int PACK, int NT>
-constexpr int stages_for() { return PACK == 1 ? STEEL_STAGES_SINGLE : STEEL_STAGES; }
+template <int PACK>
+constexpr int stages_for() { return PACK == 1 ? 2 : 4; }
 
-// Rows per wave: 32 (NT = 1), so that two waves share each SIMD and one can
-// issue MFMAs while the other computes exponentials.
-template <int D>
-constexpr int nt_for() { return STEEL_NT; }
-
-
-// Workgroup = PACK heads x 64 query rows.  Each wave owns NT 32-row MFMA
-// N-tiles of one head: NT = 2 (one wave per head; every K/V fragment read from
-// LDS feeds two MFMAs; the wave needs most of the register file) or NT = 1
-// (two waves per head, half the registers, so two waves share a SIMD).
-// RAGGED: S_k is not a multiple of the block (the tail block's copies clamp
-// their rows); without it that path is compiled out.
-template <int D, int PACK, int NT, bool RAGGED>
-__global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
+// Workgroup = PACK heads x 64 query rows.  Each wave owns 32 query rows (one
+// 32-row MFMA N-tile) of one head, two waves per head, so that two waves
+// share each SIMD and one can issue MFMAs while the other computes
+// exponentials.  RAGGED: S_k is not a multiple of the block (the tail block's
+// copies clamp their rows); without it that path is compiled out.
+template <int D, int PACK, bool RAGGED>
+__global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
+  constexpr int NT = 1;            // 32-row N-tiles per wave
   constexpr int WPH = 2 / NT;      // waves per head
   constexpr int NW = PACK * WPH;   // waves
   constexpr int C = D / 8;         // 16-byte chunks per row
@@ -78,7 +59,7 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
   static_assert(LPW >= 1 && C % NW == 0, "tile copy split");
   // A ring of ST stages, each holding the K and the V tile of one key block:
   // tiles i+1 .. i+ST-1 are being copied in while tile i is computed on.
-  constexpr int ST = stages_for<D, PACK, NT>();
+  constexpr int ST = stages_for<PACK>();
   __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
 
   // index data is read-only during the kernel: scalar loads
@@ -421,18 +402,15 @@ __global__ __launch_bounds__(64 * PACK * (2 / NT)) void k_attn(AttnArgs a) {
 
 template <int D, int PACK>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
-  constexpr int NT = nt_for<D>();
   if (grid <= 0) return;
   // At D = 64 the copy of the kernel without the ragged path needs fewer
   // registers (162 vs 178), so a third wave fits on each SIMD, and it ran
   // 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps the one
   // variant.
   if (D == 64 || a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, NT, true>), dim3(xcd_grid(grid)),
-                       dim3(64 * PACK * (2 / NT)), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(xcd_grid(grid)), dim3(128 * PACK), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<D, PACK, NT, false>), dim3(xcd_grid(grid)),
-                       dim3(64 * PACK * (2 / NT)), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(xcd_grid(grid)), dim3(128 * PACK), 0, s, a);
 }
 
 template <int D>
@@ -442,8 +420,8 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
     ap.order = w.order_p;
     ap.n_items = w.n_items + 1;
     if (p.pack == 2) launch_one<D, 2>(ap, p.NP, s);
-    else if (D == 128 && STEEL_W64 && (size_t)p.S_q * D * 4 < (1ull << 31))
-      launch_attention_w64(ap, s);
+    else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31))
+      launch_attention_ws(ap, s);
     else launch_one<D, 4>(ap, p.NP, s);
   }
   if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item

@@ -17,8 +17,11 @@ HEADER = os.path.join(ROOT, "include", "steel.h")
 FAKE = 0x100000  # 16-byte aligned, never dereferenced on the checked paths
 
 
-def declared_functions():
-    text = open(HEADER).read()
+BENCH_HEADER = os.path.join(ROOT, "include", "steel_bench.h")
+
+
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(steel_[a-z_]+)\s*\(", text)))
 
@@ -27,8 +30,15 @@ def test_library_exports_every_declared_symbol():
     lib = _lib.load()
     names = declared_functions()
     assert {"steel_attn_fwd", "steel_block_index", "steel_last_error", "steel_version"} <= set(names)
-    for name in names:
-        assert hasattr(lib, name), f"{name} declared in steel.h but not exported"
+    for name in names + declared_functions(BENCH_HEADER):
+        assert hasattr(lib, name), f"{name} declared in include/ but not exported"
+
+
+def test_mfma_peak_rejects_invalid_before_launch():
+    lib = _lib.load()
+    assert lib.steel_mfma_peak(None, 10, 256, 4, FAKE, FAKE, None) == 1
+    assert lib.steel_mfma_peak(FAKE, 0, 256, 4, FAKE, FAKE, None) == 1
+    assert lib.steel_mfma_peak(FAKE, 10, 256, 17, FAKE, FAKE, None) == 1
 
 
 def test_version_and_empty_error():
