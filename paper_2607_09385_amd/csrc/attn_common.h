@@ -30,6 +30,7 @@ struct AttnArgs {
   const int32_t* order;
   const int32_t* n_items;   // this list's item count
   const int32_t* header;    // plan header (after the two counts)
+  const int32_t* bucket;    // single-head list by XCD bucket, or nullptr
   int B, Hq, Hkv, S_q, S_k, nQB, nKB, G, causal, delta, R, pack;
   float c;  // scale * log2(e)
 };

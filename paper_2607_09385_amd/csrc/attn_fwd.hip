@@ -64,9 +64,20 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 
   // index data is read-only during the kernel: scalar loads
   if (!plan_matches(a)) return;  // index planned for another problem: out untouched
-  const int idx = xcd_slot((int)blockIdx.x);
-  if (idx >= ((cint_p)a.n_items)[0]) return;
-  const int item = ((cint_p)a.order)[idx];
+  int item;
+  if (PACK == 1 && a.bucket != nullptr) {
+    // single-head items: workgroup b runs on XCD b % 8 and takes the
+    // (b / 8)-th item of that XCD's bucket (heaviest first within it)
+    const cint_p bk = (cint_p)a.bucket;
+    const int x = (int)blockIdx.x & (kBuckets - 1), j = (int)blockIdx.x / kBuckets;
+    const int lo = bk[x];
+    if (j >= bk[x + 1] - lo) return;
+    item = bk[kBuckets + 1 + lo + j];
+  } else {
+    const int idx = xcd_slot((int)blockIdx.x);
+    if (idx >= ((cint_p)a.n_items)[0]) return;
+    item = ((cint_p)a.order)[idx];
+  }
   const int qb = item % a.nQB;
   const int bh0 = (item / a.nQB) * PACK;  // b*Hq + first head
   const int b = bh0 / a.Hq;
@@ -403,14 +414,16 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 template <int D, int PACK>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   if (grid <= 0) return;
+  // the bucket-dealt single-head list: grid is already 8 x (largest bucket)
   // At D = 64 the copy of the kernel without the ragged path needs fewer
   // registers (162 vs 178), so a third wave fits on each SIMD, and it ran
   // 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps the one
   // variant.
+  const int g = PACK == 1 && a.bucket != nullptr ? grid : xcd_grid(grid);
   if (D == 64 || a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(xcd_grid(grid)), dim3(128 * PACK), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(g), dim3(128 * PACK), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(xcd_grid(grid)), dim3(128 * PACK), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(g), dim3(128 * PACK), 0, s, a);
 }
 
 template <int D>
@@ -427,7 +440,15 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
   if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item
   a.order = w.order_s;
   a.n_items = w.n_items;
-  launch_one<D, 1>(a, p.R, s);
+  a.bucket = w.bucket;
+  int grid = p.R;
+  if (w.bucket != nullptr) {
+    // at most the rows of the key/value heads of one bucket: nQB * G rows per
+    // head, ceil(B*Hkv / 8) heads per bucket
+    const long long per = (long long)p.nQB * p.G * ((p.B * p.Hkv + kBuckets - 1) / kBuckets);
+    grid = (int)(kBuckets * per);
+  }
+  launch_one<D, 1>(a, grid, s);
 }
 
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
@@ -445,6 +466,7 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.order = nullptr;
   a.n_items = nullptr;
   a.header = w.n_items + kPlanAt;
+  a.bucket = nullptr;
   a.nKB = p.nKB;
   a.B = p.B;
   a.R = p.R;

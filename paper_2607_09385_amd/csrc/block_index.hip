@@ -376,6 +376,52 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
   order[base[hist_at(bin, c, nch, top)] + rank] = item;
 }
 
+// Stable partition of the single-head work order into the XCD buckets
+// (one 1024-thread workgroup): thread t counts the buckets of a contiguous
+// chunk of the order, one exclusive scan over the bucket-major count table
+// gives every (bucket, thread) its output position, then each thread places
+// its items.  Within a bucket the items keep the heaviest-first order.
+__global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
+                                                 const int32_t* __restrict__ n_items,
+                                                 int32_t* __restrict__ bucket) {
+  __shared__ int tab[kBuckets * 1024];
+  __shared__ int sh[32];
+  const int t = threadIdx.x;
+  const int n = n_items[0];
+  const int per = (n + 1023) / 1024;
+  const int lo = min(t * per, n), hi = min(lo + per, n);
+  auto bucket_of = [&](int r) {
+    const int bh = r / p.nQB;
+    const int b = bh / p.Hq, h = bh - b * p.Hq;
+    return (b * p.Hkv + h / p.G) & (kBuckets - 1);
+  };
+  int c[kBuckets];
+#pragma unroll
+  for (int k = 0; k < kBuckets; ++k) c[k] = 0;
+  for (int i = lo; i < hi; ++i) {
+    const int k = bucket_of(order[i]);
+#pragma unroll
+    for (int kk = 0; kk < kBuckets; ++kk) c[kk] += kk == k;
+  }
+#pragma unroll
+  for (int k = 0; k < kBuckets; ++k) tab[k * 1024 + t] = c[k];
+  __syncthreads();
+  const int total = wg_scan_array(tab, kBuckets * 1024, sh);
+  if (t < kBuckets) bucket[t] = tab[t * 1024];
+  if (t == 0) bucket[kBuckets] = total;
+  int pos[kBuckets];
+#pragma unroll
+  for (int k = 0; k < kBuckets; ++k) pos[k] = tab[k * 1024 + t];
+  int32_t* list = bucket + kBuckets + 1;
+  for (int i = lo; i < hi; ++i) {
+    const int item = order[i];
+    const int k = bucket_of(item);
+#pragma unroll
+    for (int kk = 0; kk < kBuckets; ++kk)
+      if (kk == k) list[pos[kk]++] = item;
+  }
+}
+
 hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const IndexBuffers& w,
                               hipStream_t s) {
   const int wide = mask == nullptr || ((p.nKB % 4) == 0 && ((uintptr_t)mask & 3u) == 0);
@@ -396,6 +442,8 @@ hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const Index
   hipLaunchKernelGGL(k_fill_scatter, dim3(rows_grid + nch_s + nch_p), dim3(256), 0, s, p, mask,
                      wide, w.cnt, w.row_ptr, w.col, w.hist_s, w.hist_p, w.n_items, w.order_s,
                      w.order_p, rows_grid, nch_s);
+  if (w.bucket != nullptr)
+    hipLaunchKernelGGL(k_bucket, dim3(1), dim3(1024), 0, s, p, w.order_s, w.n_items, w.bucket);
   return hipGetLastError();
 }
 

@@ -55,7 +55,16 @@ struct IndexBuffers {
   int32_t* order_p;    // [NP]  head-pack items, heaviest first
   int32_t* n_items;    // [kHeaderInts] {single items, pack items, plan header,
                        //   top bins of the two lists} (see kPlanAt, kTopBin)
+  // single-head items dealt to the 8 XCDs by key/value head (nullptr: none):
+  // [kBuckets + 1] bucket starts, then the items of order_s stably
+  // partitioned by bucket
+  int32_t* bucket;
 };
+
+// XCD buckets of single-head items: bucket (b*Hkv + g) % kBuckets, so that the
+// workgroups of one XCD read the key/value tensors of only a few heads and
+// its L2 keeps them.
+constexpr int kBuckets = 8;
 
 // Plan header written after the two item counts; the attention kernels check
 // it against their own arguments before touching the index, so a run with

@@ -177,7 +177,8 @@ int check_shape(int B, int Hq, int Hkv, int S_q, int S_k, int blk, int causal,
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct Layout {
-  size_t cnt, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, total;
+  size_t cnt, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, bucket, total;
+  bool has_bucket;  // the single-head list is also dealt into XCD buckets
 };
 
 Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
@@ -199,6 +200,8 @@ Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
     L.row_ptr = take(sizeof(int32_t) * (p.R + 1));
     L.col = take(sizeof(uint32_t) * (size_t)p.R * p.nKB);
     L.order_s = take(sizeof(int32_t) * p.R);
+    L.bucket = take(sizeof(int32_t) * ((size_t)p.R + steel::kBuckets + 1));
+    L.has_bucket = true;
   }
   L.total = off;
   return L;
@@ -248,7 +251,7 @@ int set_window(steel::Problem* p, int window_blocks, int sink_blocks) {
 }
 
 steel::IndexBuffers carve(char* ws, const Layout& L) {
-  steel::IndexBuffers w;
+  steel::IndexBuffers w{};
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
   w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
@@ -257,6 +260,7 @@ steel::IndexBuffers carve(char* ws, const Layout& L) {
   w.row_ptr = reinterpret_cast<int32_t*>(ws + L.row_ptr);
   w.col = reinterpret_cast<uint32_t*>(ws + L.col);
   w.order_s = reinterpret_cast<int32_t*>(ws + L.order_s);
+  w.bucket = L.has_bucket ? reinterpret_cast<int32_t*>(ws + L.bucket) : nullptr;
   return w;
 }
 
@@ -509,7 +513,7 @@ int steel_block_index(const uint8_t* block_mask, int B, int Hq, int S_q, int S_k
   StreamScratch* slot = nullptr;
   char* ws = nullptr;
   if ((rc = scratch_begin(dev, s, L.total, &lk, &slot, &ws)) != STEEL_OK) return rc;
-  steel::IndexBuffers w;
+  steel::IndexBuffers w{};
   w.cnt = reinterpret_cast<int32_t*>(ws + L.cnt);
   w.hist_s = reinterpret_cast<int32_t*>(ws + L.hist_s);
   w.hist_p = reinterpret_cast<int32_t*>(ws + L.hist_p);
