@@ -24,9 +24,9 @@
 // 16-lane 4x16 -> 16x4 transpose delivers exactly those keys per d column.
 //
 // A workgroup handles one work item: either one (b, h, qb) query block
-// (2 waves, 64 rows) or a pack of PACK query heads of one key/value group
-// that share the same live list (2*PACK waves), so each K/V tile is loaded
-// once for up to 256 query rows.
+// (4 waves: two row halves times two key halves of every tile) or a pack of
+// PACK query heads of one key/value group that share the same live list
+// (2*PACK waves), so each K/V tile is loaded once for up to 256 query rows.
 #include <climits>
 
 #include "attn_common.h"
@@ -39,16 +39,86 @@ namespace steel {
 template <int PACK>
 constexpr int stages_for() { return PACK == 1 ? 2 : 4; }
 
+// End of a key-split single-head workgroup: the waves of the two key halves of
+// one row half hold (m_h, l_h, O_h) over their keys, with O_h = sum 2^(s - m_h) v
+// and l_h the sum of the same weights.  With M = max(m_0, m_1) and
+// w_h = 2^(m_h - M) (0 for a half that saw no key) the row's state is
+// l = w_0 l_0 + w_1 l_1, O = w_0 O_0 + w_1 O_1.  Each wave finishes half of the
+// d tiles: it leaves the other half of its O, its m and its row sum in LDS
+// (free once the loop's last barrier has passed), and reads its partner's.
+// LDS per record: [field][lane] floats, record (row half, key half).
+template <int D>
+__device__ __forceinline__ void merge_halves(const AttnArgs& a, f32x16 (&o)[D / 32], float m,
+                                             float l, int kh, int rh, int lane, float* xs, int b,
+                                             int head, int qrow0, int hf) {
+  constexpr int DT = D / 32, HD = DT / 2;  // d tiles, d tiles finished per wave
+  constexpr int F = 2 + 16 * HD;           // fields per record
+  const float lt = half_pair_sum(l);
+  float* mine = xs + (rh * 2 + kh) * F * 64 + lane;
+  const float* part = xs + (rh * 2 + (kh ^ 1)) * F * 64 + lane;
+  // d tiles [0, HD) are finished by key half 0, [HD, DT) by key half 1 (the
+  // register array is only indexed by constants: selects, not scratch)
+  mine[0] = m;
+  mine[64] = lt;
+#pragma unroll
+  for (int j = 0; j < HD; ++j) {
+    const f32x16 give = kh ? o[j] : o[HD + j];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mine[(2 + 16 * j + r) * 64] = give[r];
+  }
+  __syncthreads();
+  const float mp = part[0], ltp = part[64];
+  const float M = fmaxf(m, mp);
+  const float w = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M);
+  const float wp = mp == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mp - M);
+  const float ls = w * lt + wp * ltp;
+  const float inv = ls > 0.f ? 1.f / ls : 0.f;
+  const int qrow = qrow0;
+  if (qrow >= a.S_q) return;
+  // log sum_j exp(scale s_ij) = (M + log2 l) ln 2 (Algorithm 1's statistics)
+  if (a.lse != nullptr && hf == 0 && kh == 0)
+    a.lse[((size_t)b * a.Hq + head) * a.S_q + qrow] =
+        ls > 0.f ? (M + log2f(ls)) * 0.69314718055994531f : -INFINITY;
+  const size_t at = (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
+#pragma unroll
+  for (int j = 0; j < HD; ++j) {
+    const int dt = kh * HD + j;
+    const f32x16 keep = kh ? o[HD + j] : o[j];
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      f32x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = 4 * gq + e;
+        v[e] = (w * keep[r] + wp * part[(2 + 16 * j + r) * 64]) * inv;
+      }
+      if (a.out_bf16) {
+        const bf16x4 vb = {(__bf16)v[0], (__bf16)v[1], (__bf16)v[2], (__bf16)v[3]};
+        *(bf16x4*)((__bf16*)a.out + at + 32 * dt + 8 * gq) = vb;
+      } else {
+        *(f32x4*)(a.out + at + 32 * dt + 8 * gq) = v;
+      }
+    }
+  }
+}
+
 // Workgroup = PACK heads x 64 query rows.  Each wave owns 32 query rows (one
 // 32-row MFMA N-tile) of one head, two waves per head, so that two waves
 // share each SIMD and one can issue MFMAs while the other computes
-// exponentials.  RAGGED: S_k is not a multiple of the block (the tail block's
-// copies clamp their rows); without it that path is compiled out.
+// exponentials.  A single head at D = 128 (whose register use allows one
+// such workgroup per SIMD pair only) would leave one wave per SIMD, so there
+// the keys of every tile are split as well: waves 0-1 take keys 0-31, waves
+// 2-3 keys 32-63, each with its own softmax state, and the two states of a
+// row are merged at the end (the split-key form of the same recurrence, exact
+// up to rounding).  At D = 64 several two-wave workgroups share a CU already.
+// RAGGED: S_k is not a multiple of the block (the
+// tail block's copies clamp their rows); without it that path is compiled out.
 template <int D, int PACK, bool RAGGED>
-__global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void k_attn(AttnArgs a) {
   constexpr int NT = 1;            // 32-row N-tiles per wave
-  constexpr int WPH = 2 / NT;      // waves per head
-  constexpr int NW = PACK * WPH;   // waves
+  constexpr int KH = PACK == 1 && D == 128 ? 2 : 1;  // key halves (waves per 32 rows)
+  constexpr int NSG = 2 / KH;      // 32-key sub-tiles per wave and tile
+  constexpr int NW = PACK * 2 * KH;  // waves
   constexpr int C = D / 8;         // 16-byte chunks per row
   constexpr int TE = kBlk * D;     // bf16 elements per tile
   constexpr int TB = TE * 2;       // bytes per tile
@@ -85,9 +155,10 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
   const int g = h0 / a.G;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int head = h0 + wave / WPH;
+  const int kh = KH == 1 ? 0 : wave >> 1;  // key half of this wave
+  const int head = h0 + (KH == 1 ? wave >> 1 : 0);
   const int n = lane & 31, hf = lane >> 5;
-  const int qrow0 = qb * kBlk + (wave % WPH) * 32 + n;  // N-tile nt holds row qrow0 + 32*nt
+  const int qrow0 = qb * kBlk + (wave & 1) * 32 + n;  // N-tile nt holds row qrow0 + 32*nt
 
   const int r0 = bh0 * a.nQB + qb;
   const int beg = ((cint_p)a.row_ptr)[r0];
@@ -129,13 +200,14 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
   };
 
   // Per-lane LDS read offsets in bytes (tile buffer base and the row block of
-  // each fragment are compile-time immediates):
+  // each fragment are compile-time immediates; a key-half wave adds its half):
   //   K fragment (sg, ks): row 32*sg + n, chunk (2*ks + hf)
   //   V fragment (sg, t, cc, dt): row 32*sg + 16*t + 8*cc + 4*(tg>>1) + tr,
   //                               chunk 4*dt + 2*(tg&1) + (tq>>1), half tq&1
+  const uint32_t half_off = (uint32_t)(kh * 32 * D * 2);
   uint32_t koff[KS];
 #pragma unroll
-  for (int ks = 0; ks < KS; ++ks) koff[ks] = (uint32_t)tile_elem<D>(n, 2 * ks + hf) * 2;
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = (uint32_t)tile_elem<D>(n, 2 * ks + hf) * 2 + half_off;
   const int tg = lane >> 4, tr = (lane >> 2) & 3, tq = lane & 3;
   uint32_t voff[2][DT];
 #pragma unroll
@@ -143,7 +215,8 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
       const int row = 8 * cc + 4 * (tg >> 1) + tr;
-      voff[cc][dt] = (uint32_t)(tile_elem<D>(row, 4 * dt + 2 * (tg & 1) + (tq >> 1)) + 4 * (tq & 1)) * 2;
+      voff[cc][dt] =
+          (uint32_t)(tile_elem<D>(row, 4 * dt + 2 * (tg & 1) + (tq >> 1)) + 4 * (tq & 1)) * 2 + half_off;
     }
 
   // Prologue.  Tile 0 is copied in while Q is fetched; the Q fragments are
@@ -247,20 +320,20 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
     }
 
     // S^T = K Q^T; K fragments read one step ahead of their MFMAs
-    f32x16 sc[NT][2];
+    f32x16 sc[NT][NSG];
     {
-      bf16x8 kf[2][2];
-      kf[0][0] = ld_k(S, 0, 0);
-      kf[0][1] = ld_k(S, 1, 0);
+      bf16x8 kf[2][NSG];
+#pragma unroll
+      for (int sg = 0; sg < NSG; ++sg) kf[0][sg] = ld_k(S, sg, 0);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int cb = ks & 1;
         if (ks + 1 < KS) {
-          kf[cb ^ 1][0] = ld_k(S, 0, ks + 1);
-          kf[cb ^ 1][1] = ld_k(S, 1, ks + 1);
+#pragma unroll
+          for (int sg = 0; sg < NSG; ++sg) kf[cb ^ 1][sg] = ld_k(S, sg, ks + 1);
         }
 #pragma unroll
-        for (int sg = 0; sg < 2; ++sg)
+        for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt) {
             if (ks == 0) sc[nt][sg] = f32x16{};
@@ -277,9 +350,9 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const int lim_abs = min(a.causal ? qrow0 + 32 * nt + a.delta : INT_MAX - kBlk, a.S_k - 1);
-        const int lim = lim_abs - (kb * kBlk + 4 * hf);
+        const int lim = lim_abs - (kb * kBlk + 4 * hf + 32 * kh);
 #pragma unroll
-        for (int sg = 0; sg < 2; ++sg)
+        for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int off = 32 * sg + 8 * (r >> 2) + (r & 3);
@@ -296,7 +369,7 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
     for (int nt = 0; nt < NT; ++nt) {
       float mx = -INFINITY;
 #pragma unroll
-      for (int sg = 0; sg < 2; ++sg)
+      for (int sg = 0; sg < NSG; ++sg)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[nt][sg][r]);
       mx = other_half_max(mx);
@@ -320,7 +393,7 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
 
-    // P.V in four phases, one per 16-key chunk k = (sg, t): phase k runs the
+    // P.V in 2*NSG phases, one per 16-key chunk k = (sg, t): phase k runs the
     // MFMAs of chunk k while the exponentials of chunk k+1 are computed and
     // the V fragments of chunk k+1 are read.  The row sums add the
     // bf16-rounded P that the MFMAs consume (v_dot2 against (1, 1)), so
@@ -342,10 +415,11 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) vf[0][dt] = ld_v(S, 0, 0, dt);
     exps(0, pa[0]);
+    constexpr int NCH = 2 * NSG;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < NCH; ++k) {
       const int cur = k & 1, nx = cur ^ 1;
-      if (k < 3) {
+      if (k + 1 < NCH) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) vf[nx][dt] = ld_v(S, (k + 1) >> 1, (k + 1) & 1, dt);
         exps(k + 1, pa[nx]);
@@ -382,6 +456,10 @@ __global__ __launch_bounds__(128 * PACK) void k_attn(AttnArgs a) {
     else if (u == 2) step(i, Par<(2 % ST)>{});
   }
 
+  if constexpr (KH == 2) {
+    merge_halves<D>(a, o[0], m[0], l[0], kh, wave & 1, lane, (float*)smem, b, head, qrow0, hf);
+    return;
+  }
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     const int qrow = qrow0 + 32 * nt;
@@ -420,10 +498,11 @@ static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   // 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps the one
   // variant.
   const int g = PACK == 1 && a.bucket != nullptr ? grid : xcd_grid(grid);
+  const int threads = PACK == 1 && D == 128 ? 256 : 128 * PACK;
   if (D == 64 || a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(g), dim3(128 * PACK), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(g), dim3(threads), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(g), dim3(128 * PACK), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(g), dim3(threads), 0, s, a);
 }
 
 template <int D>
