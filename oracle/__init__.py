@@ -16,7 +16,10 @@ It is written from the paper's definitions, independently of the GPU code:
 * ``block_select`` -- the mask producer that runs before the pass: top-k key
   blocks per query block by mean-pooled query/key score, plus the diagonal;
 * ``lse_merge``   -- the per-row log-sum-exp of the scores and the rule that
-  merges partial results computed over disjoint key chunks.
+  merges partial results computed over disjoint key chunks;
+* ``fp8_attention`` -- a float64 model of the library's fp8 (E4M3) form:
+  Algorithm 1's online recurrence with both products taking E4M3 operands
+  under power-of-two scales (an extension of Section II-C's bf16 datapath).
 
 Every function is pinned by tests against things other than itself: brute
 force on tiny inputs, closed forms, invariants and an independent library
@@ -26,3 +29,4 @@ from .masked_attention import attention, attention_rows, element_visibility, kv_
 from .block_index import N_BINS, build_index, count_bin, tile_classes, work_order  # noqa: F401
 from .block_select import block_means, block_scores, keep_count, topk_meanpool_mask  # noqa: F401
 from .lse_merge import attention_lse, merge_partials  # noqa: F401
+from .fp8_attention import attention_fp8, e4m3_round, pow2_scale  # noqa: F401
