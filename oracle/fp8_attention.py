@@ -26,6 +26,10 @@ Everything else is float64:
   O      = alpha O + E4M3(P) V8 / s_v
   out    = O / l (0 for a row with no visible key);  lse = (m - 8 + log2 l) ln 2.
 
+With ``qk_fp8=False`` (the library's P V-only fp8 form) Q and K are not
+quantized: S = (Q K^T) * scale * log2(e) from the bf16 values, and only V and
+P take E4M3 operands.
+
 Visibility is that of ``masked_attention`` (block mask and causal limit).  A
 live tile in which a row sees no key leaves that row's state unchanged, so
 iterating over the key blocks in which the row block sees any key is the
@@ -89,7 +93,8 @@ def quantize_tensor(x: np.ndarray):
 
 def _block_rows(q8, sq, k8, sk, v8, sv, vis, c):
     """One query block of one head: q8 [R, D] with scales sq [R], k8/v8
-    [S_k, D], vis [R, S_k], c = scale * log2(e).  Returns (O / l, lse)."""
+    [S_k, D] with scales sk, sv, vis [R, S_k], c = scale * log2(e).  Returns
+    (O / l, lse).  Unquantized operands come with scale 1."""
     R, S_k = vis.shape
     D = q8.shape[1]
     m = np.full(R, -np.inf)
@@ -117,10 +122,11 @@ def _block_rows(q8, sq, k8, sk, v8, sv, vis, c):
 
 
 def attention_fp8(q, k, v, block_mask=None, scale=None, causal=True, blk=64, causal_offset=None,
-                  heads=None, qblocks=None):
+                  heads=None, qblocks=None, qk_fp8=True):
     """fp8 model of the fused pass.  Returns (out, lse): float64
     [B, Hq, S_q, D] and [B, Hq, S_q]; rows outside the selected ``heads``
-    ((b, h) pairs) or ``qblocks`` (query-block indices) are NaN."""
+    ((b, h) pairs) or ``qblocks`` (query-block indices) are NaN.
+    ``qk_fp8``: Q and K in E4M3 too (else only P and V)."""
     if blk != 64:
         raise ValueError("the model follows the library's 64 x 64 tiles")
     qf, kf, vf = _f64(q), _f64(k), _f64(v)
@@ -139,7 +145,7 @@ def attention_fp8(q, k, v, block_mask=None, scale=None, causal=True, blk=64, cau
     for b, h in pairs:
         g = kv_head(h, Hq, Hkv)
         if (b, g) not in kv:
-            k8, sk = quantize_tensor(kf[b, g])
+            k8, sk = quantize_tensor(kf[b, g]) if qk_fp8 else (kf[b, g], 1.0)
             v8, sv = quantize_tensor(vf[b, g])
             kv[(b, g)] = (k8, sk, v8, sv)
         k8, sk, v8, sv = kv[(b, g)]
@@ -147,7 +153,10 @@ def attention_fp8(q, k, v, block_mask=None, scale=None, causal=True, blk=64, cau
             rows = np.arange(qb * blk, min((qb + 1) * blk, S_q))
             vis = element_visibility(None if mask is None else mask[b, h], rows, S_q, S_k, blk,
                                      causal, offset)
-            q8, sq = quantize_rows(qf[b, h, rows])
+            if qk_fp8:
+                q8, sq = quantize_rows(qf[b, h, rows])
+            else:
+                q8, sq = qf[b, h, rows], np.ones(len(rows))
             o, ls = _block_rows(q8, sq, k8, sk, v8, sv, vis, c)
             out[b, h, rows] = o
             lse[b, h, rows] = ls

@@ -176,6 +176,29 @@ def test_close_to_exact_attention_but_not_equal():
     assert np.all(out[0, 0, 64:128] == 0) and np.all(lse[0, 0, 64:128] == -np.inf)
 
 
+def test_pv_only_form():
+    # scores from the unrounded bf16 values: a single tile against loops
+    q, k, v = _inputs(1, 1, 1, 30, 30, 8, 13, spread=3.0)
+    out, lse = attention_fp8(q, k, v, scale=0.3, qk_fp8=False)
+    qd, kd, vd = (t[0, 0].double().numpy() for t in (q, k, v))
+    v8, sv = quantize_tensor(vd)
+    c = 0.3 * math.log2(math.e)
+    for i in (0, 7, 29):
+        s_ = [float(np.dot(qd[i], kd[j])) * c for j in range(i + 1)]
+        mx = max(s_)
+        p = [2.0 ** (x - mx + 8) for x in s_]
+        want = sum(float(e4m3_round(p[j])) * v8[j] for j in range(i + 1)) / sv / sum(p)
+        np.testing.assert_allclose(out[0, 0, i], want, rtol=1e-12, atol=1e-14)
+        assert lse[0, 0, i] == pytest.approx(math.log(sum(2.0 ** x for x in s_)), rel=1e-12)
+    # peaked scores (large |s|): the P V-only form stays near exact attention,
+    # the form with E4M3 scores does not
+    q, k, v = _inputs(1, 2, 2, 128, 128, 64, 15, spread=4.0)
+    exact = attention(q, k, v, None, causal=True)
+    err_pv = np.abs(attention_fp8(q, k, v, qk_fp8=False)[0] - exact)
+    err_all = np.abs(attention_fp8(q, k, v)[0] - exact)
+    assert err_pv.mean() < 0.5 * err_all.mean()
+
+
 def test_subset_rows_equal_full_run():
     q, k, v = _inputs(2, 2, 1, 150, 150, 16, 11)
     full, lse = attention_fp8(q, k, v)
