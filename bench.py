@@ -388,6 +388,26 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
         structured_b16 = {"call": "steel_attn_fwd_ex (bf16 output, with lse)",
                           "ms_per_step": round(wall_b * 1e3, 4),
                           "effective_tflops": round(f_live / wall_b / 1e12, 2)}
+    # the fp8 forms of the same call (E4M3 operands for P V, or for both
+    # products; each has its own error budget against exact attention)
+    fp8 = {}
+    lse32 = torch.empty((cfg.B, cfg.Hq, cfg.S_q), dtype=torch.float32, device=dev)
+    for mode, flag, what in (("pv", "STEEL_FP8_PV", "P V"), ("all", "STEEL_FP8", "both products")):
+        def step_f(mode=mode):
+            steel.attn_fwd_lse(qd, kd, vd, md, scale=cfg.scale, causal=cfg.causal, out=out,
+                               lse=lse32, fp8=mode)
+        for _ in range(warmup):
+            step_f()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step_f()
+        torch.cuda.synchronize()
+        wall_f = (time.perf_counter() - t0) / steps
+        fp8[mode] = {"call": f"steel_attn_fwd_ex ({flag}, with lse)",
+                     "dtype": f"E4M3 operands for {what}, fp32 accumulation",
+                     "ms_per_step": round(wall_f * 1e3, 4),
+                     "effective_tflops": round(f_live / wall_f / 1e12, 2)}
     line = {
         "metric": METRIC,
         "value": round(f_live / wall / 1e12, 2),
@@ -446,6 +466,7 @@ def bench_workload(name, steps, warmup, cpu_seconds, want_cpu, clock_warmup=0.5)
                                  "peak": 8000.0, "unit": "GB/s",
                                  "frac": round(nbytes / t_m / 1e9 / 8000.0, 4),
                                  "algorithmic_bytes": nbytes}}
+    line["fp8"] = fp8
     if structured is not None:
         line["structured_mask"] = structured
     if structured_b16 is not None:

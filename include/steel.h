@@ -160,18 +160,47 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out,
  *                  a chunk [k0, k1) of a sequence of S_k_total keys is passed
  *                  as its own K, V with causal_offset = S_k_total - S_q - k0.
  *                  Ignored when causal == 0; otherwise within [-2^30, 2^30].
- *   out_bf16       0: out is fp32 [B][Hq][S_q][D] (as steel_attn_fwd);
- *                  1: out is bf16, each value the round-to-nearest-even of
- *                  the fp32 result (half the output bytes; the error budget
- *                  of this form is larger, see the library's design notes).
+ *   flags          0 or an OR of:
+ *     STEEL_OUT_BF16  out is bf16, each value the round-to-nearest-even of
+ *                     the fp32 result (half the output bytes); without it
+ *                     out is fp32 [B][Hq][S_q][D] as for steel_attn_fwd.
+ *     STEEL_FP8_PV    the fp8 form for P V only: the scores come from bf16
+ *                     Q and K as without flags; V and the softmax weights
+ *                     are rounded to E4M3 as described under STEEL_FP8.
+ *     STEEL_FP8       the fp8 form: both products of Algorithm 1 take E4M3
+ *                     operands (OCP 8-bit float: 4 exponent bits, 3 mantissa
+ *                     bits, largest value 448) instead of the bf16 operands
+ *                     of the paper's datapath (Section II-C), accumulating in
+ *                     fp32 as before.  Q is rounded per query row after a
+ *                     power-of-two scale that maps the row's largest |value|
+ *                     into (224, 448]; K and V likewise with one scale each
+ *                     per (batch, key/value head), found by a pre-pass over
+ *                     K and V; the softmax weights 2^(s - m + 8) (m the exact
+ *                     running row maximum, so the weights lie in (0, 256])
+ *                     are rounded for P V, while the row sum adds them
+ *                     unrounded.  Scales are divided out exactly.  The
+ *                     result follows the same recurrence with larger
+ *                     rounding: its error against exact attention is the
+ *                     form's own budget, measured per workload in the
+ *                     library's design notes, not the bf16 tolerance.  The
+ *                     E4M3 copies of K and V (B*Hkv*ceil(S_k/64)*64*D bytes
+ *                     each) live in the calling stream's scratch buffer.
+ *                     Scores of large magnitude (sharply peaked attention)
+ *                     lose the most: their absolute error grows with |s|,
+ *                     and STEEL_FP8_PV keeps them at bf16 precision.
+ *                     STEEL_FP8 together with STEEL_FP8_PV is STEEL_FP8.
  *
- * Everything else as steel_attn_fwd; with lse == NULL, causal_offset =
- * S_k - S_q and out_bf16 == 0 the output is bitwise that of steel_attn_fwd.
+ * Other flag bits: STEEL_ERR_INVALID_ARGUMENT.  Everything else as
+ * steel_attn_fwd; with lse == NULL, causal_offset = S_k - S_q and flags == 0
+ * the output is bitwise that of steel_attn_fwd.
  */
+#define STEEL_OUT_BF16 1
+#define STEEL_FP8 2
+#define STEEL_FP8_PV 4
 int steel_attn_fwd_ex(const void* q, const void* k, const void* v,
                       const uint8_t* block_mask, void* out, float* lse,
                       int B, int Hq, int Hkv, int S_q, int S_k, int D, int blk,
-                      float scale, int causal, int causal_offset, int out_bf16,
+                      float scale, int causal, int causal_offset, int flags,
                       void* stream);
 
 /*

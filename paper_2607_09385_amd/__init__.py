@@ -18,6 +18,9 @@ from . import _lib
 from ._lib import SteelError, load, last_error, version  # noqa: F401
 
 BLK = 64
+STEEL_OUT_BF16 = 1  # steel_attn_fwd_ex flags (include/steel.h)
+STEEL_FP8 = 2
+STEEL_FP8_PV = 4
 
 
 def _torch():
@@ -101,12 +104,13 @@ def attn_fwd(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal:
 
 def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, causal: bool = True,
                  causal_offset: Optional[int] = None, blk: int = BLK, out=None, lse=None,
-                 out_dtype=None, stream=None):
+                 out_dtype=None, fp8=False, stream=None):
     """``attn_fwd`` that also returns the row log-sum-exp (fp32 [B, Hq, S_q],
     natural log, -inf for rows with no visible key) and takes an explicit
     causal limit ``j <= i + causal_offset`` (default S_k - S_q).  ``out_dtype``
     torch.float32 (default) or torch.bfloat16 (the fp32 result rounded to
-    nearest even)."""
+    nearest even).  ``fp8``: False (bf16 operands), "pv" (E4M3 operands for
+    P V: STEEL_FP8_PV) or True / "all" (both products: STEEL_FP8)."""
     torch = _torch()
     for name, t in (("q", q), ("k", k), ("v", v)):
         _check_bf16(name, t)
@@ -127,6 +131,14 @@ def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, cau
                 or not block_mask.is_contiguous() or block_mask.device != q.device:
             raise ValueError(f"block_mask must be a contiguous uint8 [{B}, {Hq}, {nQB}, {nKB}] on q's device")
         mask_ptr = block_mask.data_ptr()
+    if fp8 is False or fp8 is None:
+        fp8_flag = 0
+    elif fp8 is True or fp8 == "all":
+        fp8_flag = STEEL_FP8
+    elif fp8 == "pv":
+        fp8_flag = STEEL_FP8_PV
+    else:
+        raise ValueError('fp8 must be False, "pv", True or "all"')
     odt = torch.float32 if out_dtype is None else out_dtype
     if odt not in (torch.float32, torch.bfloat16):
         raise ValueError("out_dtype must be torch.float32 or torch.bfloat16")
@@ -144,7 +156,8 @@ def attn_fwd_lse(q, k, v, block_mask=None, *, scale: Optional[float] = None, cau
         st = _lib.load().steel_attn_fwd_ex(
             q.data_ptr(), k.data_ptr(), v.data_ptr(), mask_ptr, out.data_ptr(), lse.data_ptr(),
             B, Hq, Hkv, S_q, S_k, D, blk, float(scale), 1 if causal else 0, int(causal_offset),
-            1 if odt == torch.bfloat16 else 0, _stream_handle(stream))
+            (STEEL_OUT_BF16 if odt == torch.bfloat16 else 0) | fp8_flag,
+            _stream_handle(stream))
     _lib.check(st)
     return out, lse
 

@@ -19,6 +19,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsteel.so")
 SOURCES = ["steel_api.cpp", "block_index.hip", "block_select.hip", "attn_fwd.hip", "attn_ws.hip",
+           "quant_fp8.hip",
            "attn_merge.hip", "noalloc.hip", "mfma_peak.hip"]
 ARCH = "gfx950"
 

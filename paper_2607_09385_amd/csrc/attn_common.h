@@ -31,6 +31,9 @@ struct AttnArgs {
   const int32_t* n_items;   // this list's item count
   const int32_t* header;    // plan header (after the two counts)
   const int32_t* bucket;    // single-head list by XCD bucket, or nullptr
+  const uint8_t* k8;        // fp8 form: E4M3 tiles of K and V (Fp8Buffers),
+  const uint8_t* v8;        //   nullptr in the bf16 form
+  const float* f8_scale;    //   and the per-(b, g) inverse scales {1/s_k, 1/s_v}
   int B, Hq, Hkv, S_q, S_k, nQB, nKB, G, causal, delta, R, pack;
   float c;  // scale * log2(e)
 };

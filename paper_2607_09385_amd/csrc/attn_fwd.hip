@@ -39,6 +39,32 @@ namespace steel {
 template <int PACK>
 constexpr int stages_for() { return PACK == 1 ? 2 : 4; }
 
+// Key halves per row half: a single head at D = 128 in bf16 splits every
+// tile's keys over two wave pairs (see k_attn); everything else keeps whole
+// tiles per wave.
+template <int D, int PACK, int PREC>
+constexpr int key_halves() { return PACK == 1 && D == 128 && PREC == kBf16 ? 2 : 1; }
+template <int D, int PACK, int PREC>
+constexpr int attn_threads() { return 128 * PACK * key_halves<D, PACK, PREC>(); }
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+// Four values rounded to E4M3 (nearest even), packed in memory order.
+__device__ __forceinline__ int pack_e4m3(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+}
+
+// 32 bytes of E4M3 operand from two 16-byte LDS reads.
+__device__ __forceinline__ i32x8 lds_pair(const char* p0, const char* p1) {
+  const u32x4 lo = *(const u32x4*)p0, hi = *(const u32x4*)p1;
+  return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+__device__ __forceinline__ f32x16 mfma_e4m3(const i32x8& a, const i32x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
 // End of a key-split single-head workgroup: the waves of the two key halves of
 // one row half hold (m_h, l_h, O_h) over their keys, with O_h = sum 2^(s - m_h) v
 // and l_h the sum of the same weights.  With M = max(m_0, m_1) and
@@ -113,24 +139,39 @@ __device__ __forceinline__ void merge_halves(const AttnArgs& a, f32x16 (&o)[D / 
 // up to rounding).  At D = 64 several two-wave workgroups share a CU already.
 // RAGGED: S_k is not a multiple of the block (the
 // tail block's copies clamp their rows); without it that path is compiled out.
-template <int D, int PACK, bool RAGGED>
-__global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void k_attn(AttnArgs a) {
+template <int D, int PACK, bool RAGGED, int PREC>
+__global__ __launch_bounds__((attn_threads<D, PACK, PREC>())) void k_attn(AttnArgs a) {
+  constexpr bool QK8 = PREC == kFp8All;  // S = K Q^T from E4M3 operands
+  constexpr bool PV8 = PREC != kBf16;    // O += V P from E4M3 operands
   constexpr int NT = 1;            // 32-row N-tiles per wave
-  constexpr int KH = PACK == 1 && D == 128 ? 2 : 1;  // key halves (waves per 32 rows)
+  constexpr int KH = key_halves<D, PACK, PREC>();  // key halves (waves per 32 rows)
   constexpr int NSG = 2 / KH;      // 32-key sub-tiles per wave and tile
   constexpr int NW = PACK * 2 * KH;  // waves
-  constexpr int C = D / 8;         // 16-byte chunks per row
-  constexpr int TE = kBlk * D;     // bf16 elements per tile
-  constexpr int TB = TE * 2;       // bytes per tile
-  constexpr int LPW = C / NW;      // 16-byte copies per lane per tile (per tensor)
-  constexpr int KS = D / 16;       // k-steps of S^T = K Q^T
+  constexpr int C = D / 8;         // 16-byte chunks per bf16 row
+  constexpr int TE = kBlk * D;     // elements per tile
+  constexpr int TB8 = TE;          // bytes of an E4M3 tile
+  constexpr int TBK = QK8 ? TB8 : 2 * TE, TBV = PV8 ? TB8 : 2 * TE;  // K, V tile bytes
+  constexpr int SB = TBK + TBV;    // bytes per ring stage
+  // 16-byte copies per lane per tile: bf16 tiles LPW from every wave; E4M3
+  // tiles LPW8 from the first CW8 waves
+  constexpr int LPW = C / NW;
+  constexpr int LPW8 = TB8 / 16 >= 64 * NW ? TB8 / 16 / (64 * NW) : 1;
+  constexpr int CW8 = TB8 / 16 / (64 * LPW8);
+  // copy instructions per lane per tile of waves below CW8 and of the others
+  constexpr int CPT_LO = (QK8 ? LPW8 : LPW) + (PV8 ? LPW8 : LPW);
+  constexpr int CPT_HI = (QK8 ? 0 : LPW) + (PV8 ? 0 : LPW);
+  constexpr int KS = D / 16;       // k-steps of S^T = K Q^T (bf16)
+  constexpr int KS8 = D / 64;      // k-steps of S^T = K Q^T (fp8)
   constexpr int DT = D / 32;       // d tiles of O^T
-  constexpr float TAU = 8.0f;      // rescale only when the row max grows by > 2^8
-  static_assert(LPW >= 1 && C % NW == 0, "tile copy split");
+  // bf16 P: rescale only when the row max grows by > 2^8; E4M3 P: on every
+  // growth (its weights need the exact maximum, see the P step)
+  constexpr float TAU = PV8 ? 0.0f : 8.0f;
+  static_assert(LPW >= 1 && C % NW == 0 && CW8 >= 1 && CW8 <= NW && CW8 * 64 * LPW8 * 16 == TB8,
+                "tile copy split");
   // A ring of ST stages, each holding the K and the V tile of one key block:
   // tiles i+1 .. i+ST-1 are being copied in while tile i is computed on.
   constexpr int ST = stages_for<PACK>();
-  __shared__ __attribute__((aligned(1024))) __bf16 smem[2 * ST * TE];
+  __shared__ __attribute__((aligned(1024))) char smem[ST * SB];
 
   // index data is read-only during the kernel: scalar loads
   if (!plan_matches(a)) return;  // index planned for another problem: out untouched
@@ -198,6 +239,26 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
       }
     }
   };
+  // E4M3 tiles are stored as they sit in LDS (keys past S_k zero), so a
+  // straight copy by the first CW8 waves, LPW8 16-byte pieces per lane
+  const size_t tile8 = ((size_t)b * a.Hkv + g) * a.nKB;  // first tile of this head
+  auto issue_copy8 = [&](const uint8_t* src, uint32_t dst, int kb) {
+    if (wave < CW8) {
+      const uint8_t* sb = src + (tile8 + kb) * TB8;
+      const uint32_t lbase = lds0 + dst + (uint32_t)(wave * LPW8) * 1024u;
+#pragma unroll
+      for (int j = 0; j < LPW8; ++j)
+        copy16_to_lds(sb, (uint32_t)(((wave * LPW8 + j) * 64 + lane) * 16), lbase + j * 1024u);
+    }
+  };
+  // K and V tiles of key block kb into ring stage st (K at st*SB, V after it)
+  auto copy_kv = [&](int st, int kb) {
+    const uint32_t at = (uint32_t)st * SB;
+    if constexpr (QK8) issue_copy8(a.k8, at, kb);
+    else issue_copy(kg, at, kb);
+    if constexpr (PV8) issue_copy8(a.v8, at + TBK, kb);
+    else issue_copy(vg, at + TBK, kb);
+  };
 
   // Per-lane LDS read offsets in bytes (tile buffer base and the row block of
   // each fragment are compile-time immediates; a key-half wave adds its half):
@@ -225,22 +286,48 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
   // earlier).  Left to itself it would put that wait at the first use inside
   // the loop, where it would drain every in-flight copy on each iteration.
   // Only then are tiles 1 .. ST-2 put in flight.  Stage s holds K at byte
-  // offset 2*s*TB and V at (2*s + 1)*TB.
-  constexpr int CPT = 2 * LPW;  // copy instructions per lane per tile
-  if (L > 0) {
-    const int kb = (int)(colp[0] & 0x7fffffffu);
-    issue_copy(kg, 0, kb);
-    issue_copy(vg, TB, kb);
-  }
+  // offset s*SB and V at s*SB + TBK.
+  if (L > 0) copy_kv(0, (int)(colp[0] & 0x7fffffffu));
 
   // Q rows as the B operand: N-tile nt, lane holds row 32*nt + n, d = 16*ks + 8*hf + 0..7
-  bf16x8 qf[NT][KS];
+  bf16x8 qf[QK8 ? 1 : NT][QK8 ? 1 : KS];
+  // fp8: lane holds row 32*nt + n, dims 64*ks8 + 32*hf + 0..31 as E4M3 of
+  // Q * s_q with the row's own power-of-two scale s_q; cr is the row's
+  // factor from the MFMA scores to log2 units, scale*log2(e) / (s_q s_k)
+  i32x8 q8[NT][QK8 ? KS8 : 1];
+  float cr[NT];
+  const float dv = PV8 ? a.f8_scale[2 * ((size_t)b * a.Hkv + g) + 1] : 1.f;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const __bf16* qp =
-        a.q + (((size_t)b * a.Hq + head) * a.S_q + min(qrow0 + 32 * nt, a.S_q - 1)) * D + 8 * hf;
+    const __bf16* qrow =
+        a.q + (((size_t)b * a.Hq + head) * a.S_q + min(qrow0 + 32 * nt, a.S_q - 1)) * D;
+    if constexpr (QK8) {
+      bf16x8 x[KS8][4];
+      float amax = 0.f;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qp + 16 * ks);
+      for (int ks = 0; ks < KS8; ++ks)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          x[ks][u] = *(const bf16x8*)(qrow + 64 * ks + 32 * hf + 8 * u);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)x[ks][u][e]));
+        }
+      const float sq = e4m3_scale(other_half_max(amax));
+#pragma unroll
+      for (int ks = 0; ks < KS8; ++ks)
+#pragma unroll
+        for (int w = 0; w < 8; ++w) {
+          const bf16x8& xv = x[ks][w >> 1];
+          const int e = 4 * (w & 1);
+          q8[nt][ks][w] = pack_e4m3((float)xv[e] * sq, (float)xv[e + 1] * sq, (float)xv[e + 2] * sq,
+                                    (float)xv[e + 3] * sq);
+        }
+      cr[nt] = a.c / sq * a.f8_scale[2 * ((size_t)b * a.Hkv + g)];
+    } else {
+      cr[nt] = a.c;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qrow + 8 * hf + 16 * ks);
+    }
   }
   // The live list is kept in two VGPRs (entries 64j .. 64j+127, one per
   // lane) and entries are extracted with v_readlane.  Scalar loads inside the
@@ -255,20 +342,18 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
     const int off = k - wbase;
     return (uint32_t)__builtin_amdgcn_readlane((int)(off < 64 ? win0 : win1), off & 63);
   };
+  if constexpr (!QK8) {
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt)
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qf[nt][ks]));
+      for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(qf[nt][ks]));
+  }
   asm volatile("" ::"v"(win0), "v"(win1));
   wait_vm<0>();
 
 #pragma unroll
   for (int s = 1; s < ST - 1; ++s)
-    if (s < L) {
-      const int kb = (int)(colp[s] & 0x7fffffffu);
-      issue_copy(kg, (2 * s) * TB, kb);
-      issue_copy(vg, (2 * s + 1) * TB, kb);
-    }
+    if (s < L) copy_kv(s, (int)(colp[s] & 0x7fffffffu));
 
   f32x16 o[NT][DT];
   float m[NT], l[NT];
@@ -282,13 +367,32 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
 
   const char* lds_bytes = (const char*)smem;
   auto ld_k = [&](int S, int sg, int ks) -> bf16x8 {
-    return *(const bf16x8*)(lds_bytes + 2 * S * TB + sg * 32 * D * 2 + koff[ks]);
+    return *(const bf16x8*)(lds_bytes + S * SB + sg * 32 * D * 2 + koff[ks]);
   };
   auto ld_v = [&](int S, int sg, int t, int dt) -> bf16x8 {
-    const char* base = lds_bytes + (2 * S + 1) * TB + (32 * sg + 16 * t) * D * 2;
+    const char* base = lds_bytes + S * SB + TBK + (32 * sg + 16 * t) * D * 2;
     const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[0][dt]));
     const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + voff[1][dt]));
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  // fp8 operand reads (layouts of Fp8Buffers): K fragment (sg, ks8) = row
+  // 32*sg + n, logical chunks 4*ks8 + 2*hf + {0, 1}; V fragment dt = row
+  // 32*dt + n of the transposed tile, logical chunks 2*hf + {0, 1}
+  uint32_t koff8[QK8 ? KS8 : 1][2], voff8[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+#pragma unroll
+    for (int ks = 0; ks < (QK8 ? KS8 : 1); ++ks)
+      koff8[ks][u] = (uint32_t)(n * D + 16 * ((4 * ks + 2 * hf + u) ^ kswz8<D>(n)));
+    voff8[u] = (uint32_t)(n * kBlk + 16 * ((2 * hf + u) ^ ((n >> 2) & 3)));
+  }
+  auto ld_k8 = [&](int S, int sg, int ks) -> i32x8 {
+    const char* base = lds_bytes + S * SB + sg * 32 * D;
+    return lds_pair(base + koff8[ks][0], base + koff8[ks][1]);
+  };
+  auto ld_v8 = [&](int S, int dt) -> i32x8 {
+    const char* base = lds_bytes + S * SB + TBK + dt * 32 * kBlk;
+    return lds_pair(base + voff8[0], base + voff8[1]);
   };
 
   // tile 0 has landed (waited for with Q); make it visible to every wave
@@ -314,14 +418,22 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
     const bool refill = i + ST - 1 < L;
     if (refill) {
       constexpr int SN = (S + ST - 1) % ST;
-      const int kbn = (int)(entry(i + ST - 1) & 0x7fffffffu);
-      issue_copy(kg, (2 * SN) * TB, kbn);
-      issue_copy(vg, (2 * SN + 1) * TB, kbn);
+      copy_kv(SN, (int)(entry(i + ST - 1) & 0x7fffffffu));
     }
 
     // S^T = K Q^T; K fragments read one step ahead of their MFMAs
     f32x16 sc[NT][NSG];
-    {
+    if constexpr (QK8) {
+#pragma unroll
+      for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+        for (int ks = 0; ks < KS8; ++ks) {
+          const i32x8 kf = ld_k8(S, sg, ks);
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            sc[nt][sg] = mfma_e4m3(kf, q8[nt][ks], ks == 0 ? f32x16{} : sc[nt][sg]);
+        }
+    } else {
       bf16x8 kf[2][NSG];
 #pragma unroll
       for (int sg = 0; sg < NSG; ++sg) kf[0][sg] = ld_k(S, sg, 0);
@@ -373,7 +485,7 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[nt][sg][r]);
       mx = other_half_max(mx);
-      mt[nt] = mx == -INFINITY ? -INFINITY : mx * a.c;
+      mt[nt] = mx == -INFINITY ? -INFINITY : mx * cr[nt];
       grow |= mt[nt] > m[nt] + TAU;
     }
     // Rescale only when some row's maximum grew by more than TAU (log2
@@ -392,6 +504,33 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
     float msafe[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
+
+    if constexpr (PV8) {
+      // P = 2^(S - m + 8) in (0, 2^8] (m is the exact running maximum):
+      // rounded to E4M3 for the product, summed before rounding into l; the
+      // lane's 32 weights in the operand's byte order b = 16*sg + r
+      i32x8 p8[NT];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const float mo = 8.f - msafe[nt];
+        float pv[32];
+#pragma unroll
+        for (int sg = 0; sg < NSG; ++sg)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            pv[16 * sg + r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[nt][sg][r], cr[nt], mo));
+#pragma unroll
+        for (int j = 0; j < 32; ++j) l[nt] += pv[j];
+#pragma unroll
+        for (int w = 0; w < 8; ++w) p8[nt][w] = pack_e4m3(pv[4 * w], pv[4 * w + 1], pv[4 * w + 2], pv[4 * w + 3]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const i32x8 vf = ld_v8(S, dt);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) o[nt][dt] = mfma_e4m3(vf, p8[nt], o[nt][dt]);
+      }
+    } else {
 
     // P.V in 2*NSG phases, one per 16-key chunk k = (sg, t): phase k runs the
     // MFMAs of chunk k while the exponentials of chunk k+1 are computed and
@@ -430,12 +569,18 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
         for (int nt = 0; nt < NT; ++nt)
           o[nt][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[cur][dt], pa[cur][nt], o[nt][dt], 0, 0, 0);
     }
+    }
 
     // tile i+1 must have landed before the barrier: newer copies (tiles
-    // i+2 .. i+ST-1, CPT instructions each) may stay in flight
+    // i+2 .. i+ST-1, the wave's CPT_LO or CPT_HI instructions each) may stay
+    // in flight
     if (i + 1 < L) {
-      if (i + ST - 1 < L) wait_vm<(ST - 2) * CPT>();
-      else wait_vm<0>();
+      if (i + ST - 1 < L) {
+        if (CPT_LO == CPT_HI || wave < CW8) wait_vm<(ST - 2) * CPT_LO>();
+        else wait_vm<(ST - 2) * CPT_HI>();
+      } else {
+        wait_vm<0>();
+      }
     }
     __syncthreads();  // tile i's stage may be refilled from here on
   };
@@ -464,12 +609,15 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
   for (int nt = 0; nt < NT; ++nt) {
     const int qrow = qrow0 + 32 * nt;
     const float lt = half_pair_sum(l[nt]);
-    const float inv = lt > 0.f ? 1.f / lt : 0.f;
+    // fp8: the value scale s_v is divided out here (dv = 1/s_v)
+    const float inv = lt > 0.f ? dv / lt : 0.f;
     // log sum_j exp(scale s_ij) = (m + log2 l) ln 2: m in log2 units, l the
-    // row sum relative to 2^m (Algorithm 1's statistics)
+    // row sum relative to 2^m (Algorithm 1's statistics; the fp8 weights
+    // carry an extra 2^8)
+    constexpr float m_off = PV8 ? 8.f : 0.f;
     if (a.lse != nullptr && hf == 0 && qrow < a.S_q)
       a.lse[((size_t)b * a.Hq + head) * a.S_q + qrow] =
-          lt > 0.f ? (m[nt] + log2f(lt)) * 0.69314718055994531f : -INFINITY;
+          lt > 0.f ? (m[nt] - m_off + log2f(lt)) * 0.69314718055994531f : -INFINITY;
     if (qrow < a.S_q) {
       const size_t at = (((size_t)b * a.Hq + head) * a.S_q + qrow) * D + 4 * hf;
 #pragma unroll
@@ -489,32 +637,35 @@ __global__ __launch_bounds__(128 * PACK * (PACK == 1 && D == 128 ? 2 : 1)) void 
   }
 }
 
-template <int D, int PACK>
+template <int D, int PACK, int PREC>
 static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   if (grid <= 0) return;
   // the bucket-dealt single-head list: grid is already 8 x (largest bucket)
-  // At D = 64 the copy of the kernel without the ragged path needs fewer
-  // registers (162 vs 178), so a third wave fits on each SIMD, and it ran
-  // 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps the one
-  // variant.
   const int g = PACK == 1 && a.bucket != nullptr ? grid : xcd_grid(grid);
-  const int threads = PACK == 1 && D == 128 ? 256 : 128 * PACK;
-  if (D == 64 || a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, true>), dim3(g), dim3(threads), 0, s, a);
+  constexpr int threads = attn_threads<D, PACK, PREC>();
+  // E4M3 tiles are padded with zero keys: with both tensors in E4M3 no copy
+  // clamps.  At D = 64 the copy of the bf16 kernel without the ragged path
+  // needs fewer registers (162 vs 178), so a third wave fits on each SIMD,
+  // and it ran 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps
+  // the one variant.
+  if constexpr (PREC == kFp8All)
+    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g), dim3(threads), 0, s, a);
+  else if (D == 64 || a.S_k % kBlk != 0)
+    hipLaunchKernelGGL((k_attn<D, PACK, true, PREC>), dim3(g), dim3(threads), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<D, PACK, false>), dim3(g), dim3(threads), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g), dim3(threads), 0, s, a);
 }
 
-template <int D>
+template <int D, int PREC>
 static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStream_t s) {
   if (p.pack > 1) {
     AttnArgs ap = a;
     ap.order = w.order_p;
     ap.n_items = w.n_items + 1;
-    if (p.pack == 2) launch_one<D, 2>(ap, p.NP, s);
-    else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31))
+    if (p.pack == 2) launch_one<D, 2, PREC>(ap, p.NP, s);
+    else if (D == 128 && PREC == kBf16 && (size_t)p.S_q * D * 4 < (1ull << 31))
       launch_attention_ws(ap, s);
-    else launch_one<D, 4>(ap, p.NP, s);
+    else launch_one<D, 4, PREC>(ap, p.NP, s);
   }
   if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item
   a.order = w.order_s;
@@ -527,12 +678,12 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
     const long long per = (long long)p.nQB * p.G * ((p.B * p.Hkv + kBuckets - 1) / kBuckets);
     grid = (int)(kBuckets * per);
   }
-  launch_one<D, 1>(a, grid, s);
+  launch_one<D, 1, PREC>(a, grid, s);
 }
 
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
                             float* out, float* lse, float scale, const IndexBuffers& w,
-                            hipStream_t s) {
+                            const Fp8Buffers& f, hipStream_t s) {
   AttnArgs a;
   a.q = (const __bf16*)q;
   a.k = (const __bf16*)k;
@@ -546,6 +697,9 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.n_items = nullptr;
   a.header = w.n_items + kPlanAt;
   a.bucket = nullptr;
+  a.k8 = p.fp8 ? f.k8 : nullptr;
+  a.v8 = p.fp8 ? f.v8 : nullptr;
+  a.f8_scale = p.fp8 ? f.scale : nullptr;
   a.nKB = p.nKB;
   a.B = p.B;
   a.R = p.R;
@@ -559,8 +713,16 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.causal = p.causal;
   a.delta = p.delta;
   a.c = scale * 1.4426950408889634f;
-  if (p.D == 64) launch_d<64>(p, a, w, s);
-  else launch_d<128>(p, a, w, s);
+  if (p.fp8 == kFp8All) {
+    if (p.D == 64) launch_d<64, kFp8All>(p, a, w, s);
+    else launch_d<128, kFp8All>(p, a, w, s);
+  } else if (p.fp8 == kFp8Pv) {
+    if (p.D == 64) launch_d<64, kFp8Pv>(p, a, w, s);
+    else launch_d<128, kFp8Pv>(p, a, w, s);
+  } else {
+    if (p.D == 64) launch_d<64, kBf16>(p, a, w, s);
+    else launch_d<128, kBf16>(p, a, w, s);
+  }
   return hipGetLastError();
 }
 

@@ -42,7 +42,55 @@ struct Problem {
   // then uniform and the single-head list is empty, so it is not launched.
   int heads_share_mask;
   int out_bf16;  // output in bf16 (RNE of the fp32 result) instead of fp32
+  int fp8;       // operand precision of the products: a Prec value
 };
+
+// Operand precision of Algorithm 1's two products: bf16 (the paper's AIE
+// datapath, Section II-C), E4M3 for P V only, or E4M3 for both (see
+// Fp8Buffers); accumulation is fp32 in every case.
+enum Prec { kBf16 = 0, kFp8Pv = 1, kFp8All = 2 };
+
+// Operands of the fp8 form, written by the pre-pass (quant_fp8.hip) and read
+// by the attention kernels.  Both tensors are cut into the 64-key tiles of
+// the mask, tile (b*Hkv + g, kb) at byte (b*Hkv + g) * nKB * 64 * D +
+// kb * 64 * D, keys past S_k zero; each tile is stored exactly as the
+// kernels keep it in LDS, so one straight copy moves it:
+//   k8  row r (key 64 kb + r) of D bytes E4M3(K s_k); its 16-byte chunk c
+//       (dims 16c .. 16c + 15) at chunk slot c ^ kswz(r) of the row;
+//   v8  row d of 64 bytes E4M3(V s_v) over the tile's keys in the order of
+//       the P operand (byte j = 32 h + b holds key 32 (b/16) + 8 ((b%16)/4)
+//       + 4 h + b%4); its chunk c at slot c ^ ((d >> 2) & 3).
+// The swizzles keep the 16-byte operand reads of 16 lanes on distinct LDS
+// banks.  scale: per (b*Hkv + g) the two inverse scales {1/s_k, 1/s_v};
+// part: the per-chunk maxima the scales come from.  k8 is nullptr when
+// only P V takes E4M3 operands.
+struct Fp8Buffers {
+  uint8_t* k8;
+  uint8_t* v8;
+  float* part;   // [B*Hkv][kFp8Chunks][2]
+  float* scale;  // [B*Hkv][2]
+};
+constexpr int kFp8Chunks = 32;
+constexpr float kE4M3Max = 448.f;
+
+template <int D>
+__host__ __device__ inline int kswz8(int r) {
+  return D == 128 ? (r >> 1) & 7 : (r >> 2) & 3;
+}
+
+// Power-of-two scale 2^floor(log2(448 / amax)) of a tensor whose largest
+// magnitude is amax (1 for 0 or a non-finite amax).
+__host__ __device__ inline float e4m3_scale(float amax) {
+  if (!(amax > 0.f) || !(amax <= 3.4e38f)) return 1.f;
+  const float x = kE4M3Max / amax;  // >= 1.3e-36: a normal float
+  uint32_t bits;
+  __builtin_memcpy(&bits, &x, 4);
+  bits &= 0x7f800000u;              // 2^floor(log2 x)
+  if (bits == 0x7f800000u) bits = 0x7f000000u;  // x overflowed: 2^127
+  float sc;
+  __builtin_memcpy(&sc, &bits, 4);
+  return sc;
+}
 
 // Device workspace of one call.
 struct IndexBuffers {
@@ -109,11 +157,17 @@ hipError_t launch_topk_mask(const Problem& p, const __bf16* q, const __bf16* k, 
                             int keep_den, uint8_t* mask, double* qm, double* km, double* scores,
                             hipStream_t stream);
 
+// Enqueue the fp8 pre-pass: per (b, g) maxima of |K| and |V|, their scales
+// and the E4M3 tiles of Fp8Buffers.
+hipError_t launch_fp8_prepass(const Problem& p, const void* k, const void* v, const Fp8Buffers& f,
+                              hipStream_t stream);
+
 // Enqueue the fused attention over both item lists; lse (nullable) receives
-// the row log-sum-exp [B][Hq][S_q].
+// the row log-sum-exp [B][Hq][S_q].  f: the fp8 operands when p.fp8, else
+// ignored.
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
                             float* out, float* lse, float scale, const IndexBuffers& w,
-                            hipStream_t stream);
+                            const Fp8Buffers& f, hipStream_t stream);
 
 // Enqueue the merge of n_parts partial results over disjoint key sets
 // (attn_merge.hip): o_parts [n_parts][rows][D], lse_parts [n_parts][rows].

@@ -179,6 +179,7 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct Layout {
   size_t cnt, hist_s, hist_p, row_ptr, col, order_s, order_p, n_items, bucket, total;
   bool has_bucket;  // the single-head list is also dealt into XCD buckets
+  size_t k8, v8, f8_part, f8_scale;  // fp8 operands (when Problem::fp8)
 };
 
 Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
@@ -202,6 +203,13 @@ Layout layout(const steel::Problem& p, bool with_rowptr_col_order) {
     L.order_s = take(sizeof(int32_t) * p.R);
     L.bucket = take(sizeof(int32_t) * ((size_t)p.R + steel::kBuckets + 1));
     L.has_bucket = true;
+  }
+  if (p.fp8) {
+    const size_t tiles = (size_t)p.B * p.Hkv * p.nKB * steel::kBlk * p.D;  // bytes per tensor
+    L.k8 = p.fp8 == steel::kFp8All ? take(tiles) : 0;
+    L.v8 = take(tiles);
+    L.f8_part = take(sizeof(float) * 2 * steel::kFp8Chunks * p.B * p.Hkv);
+    L.f8_scale = take(sizeof(float) * 2 * p.B * p.Hkv);
   }
   L.total = off;
   return L;
@@ -288,9 +296,17 @@ int fused_call(const steel::Problem& p, const void* q, const void* k, const void
   char* ws = nullptr;
   if ((rc = scratch_begin(dev, s, L.total, &lk, &slot, &ws)) != STEEL_OK) return rc;
   const steel::IndexBuffers w = carve(ws, L);
+  steel::Fp8Buffers f{};
+  if (p.fp8) {
+    f.k8 = p.fp8 == steel::kFp8All ? reinterpret_cast<uint8_t*>(ws + L.k8) : nullptr;
+    f.v8 = reinterpret_cast<uint8_t*>(ws + L.v8);
+    f.part = reinterpret_cast<float*>(ws + L.f8_part);
+    f.scale = reinterpret_cast<float*>(ws + L.f8_scale);
+  }
   hipError_t e = steel::launch_block_index(p, block_mask, w, s);
+  if (e == hipSuccess && p.fp8) e = steel::launch_fp8_prepass(p, k, v, f, s);
   if (e == hipSuccess)
-    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), lse, scale, w, s);
+    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), lse, scale, w, f, s);
   const int re = scratch_end(slot, dev, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   return re;
@@ -331,7 +347,7 @@ int steel_attn_fwd_window(const void* q, const void* k, const void* v, void* out
 
 int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t* block_mask,
                       void* out, float* lse, int B, int Hq, int Hkv, int S_q, int S_k, int D,
-                      int blk, float scale, int causal, int causal_offset, int out_bf16,
+                      int blk, float scale, int causal, int causal_offset, int flags,
                       void* stream) {
   g_err.clear();
   steel::Problem p{};
@@ -342,9 +358,11 @@ int steel_attn_fwd_ex(const void* q, const void* k, const void* v, const uint8_t
       return fail(STEEL_ERR_INVALID_ARGUMENT, "causal_offset %d outside [-2^30, 2^30]", causal_offset);
     p.delta = causal_offset;
   }
-  if (out_bf16 != 0 && out_bf16 != 1)
-    return fail(STEEL_ERR_INVALID_ARGUMENT, "out_bf16 must be 0 or 1 (got %d)", out_bf16);
-  p.out_bf16 = out_bf16;
+  if (flags & ~(STEEL_OUT_BF16 | STEEL_FP8 | STEEL_FP8_PV))
+    return fail(STEEL_ERR_INVALID_ARGUMENT,
+                "flags may hold only STEEL_OUT_BF16, STEEL_FP8 and STEEL_FP8_PV (got %d)", flags);
+  p.out_bf16 = (flags & STEEL_OUT_BF16) != 0;
+  p.fp8 = (flags & STEEL_FP8) ? steel::kFp8All : (flags & STEEL_FP8_PV) ? steel::kFp8Pv : steel::kBf16;
   set_pack(&p);
   p.heads_share_mask = block_mask == nullptr;
   return fused_call(p, q, k, v, block_mask, out, lse, scale, stream);
@@ -374,7 +392,8 @@ int steel_attn_fwd_noalloc(const void* q, const void* k, const void* v,
   const steel::IndexBuffers w = carve(ws, L);
   e = steel::launch_block_index(p, block_mask, w, s);
   if (e == hipSuccess)
-    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), nullptr, scale, w, s);
+    e = steel::launch_attention(p, q, k, v, static_cast<float*>(out), nullptr, scale, w,
+                                steel::Fp8Buffers{}, s);
   if (e != hipSuccess) return hip_fail(e, "launching kernels");
   return STEEL_OK;
 }
@@ -451,7 +470,7 @@ int steel_attn_run(const void* q, const void* k, const void* v, void* out, int B
   if ((rc = check_workspace(workspace, workspace_bytes, L)) != STEEL_OK) return rc;
   hipError_t e = steel::launch_attention(
       p, q, k, v, static_cast<float*>(out), nullptr, scale,
-      carve(const_cast<char*>(static_cast<const char*>(workspace)), L),
+      carve(const_cast<char*>(static_cast<const char*>(workspace)), L), steel::Fp8Buffers{},
       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "launching the attention kernels");
   return STEEL_OK;

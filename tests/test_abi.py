@@ -185,8 +185,11 @@ def test_lse_and_merge_entry_points_reject_invalid():
                                0, 0, None)
     assert st == 1 and "non-NULL" in _lib.last_error()
     st = lib.steel_attn_fwd_ex(FAKE, FAKE, FAKE, None, FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.1, 1,
-                               0, 2, None)
-    assert st == 1 and "out_bf16" in _lib.last_error()
+                               0, 8, None)
+    assert st == 1 and "flags" in _lib.last_error()
+    st = lib.steel_attn_fwd_ex(FAKE, FAKE, FAKE, None, FAKE, FAKE, 1, 4, 2, 128, 128, 64, 64, 0.1, 1,
+                               0, -1, None)
+    assert st == 1 and "flags" in _lib.last_error()
     st = lib.steel_attn_merge(FAKE, FAKE, 0, 10, 64, FAKE, None, None)
     assert st == 1 and "n_parts" in _lib.last_error()
     st = lib.steel_attn_merge(FAKE, FAKE, 2, 10, 66, FAKE, None, None)
