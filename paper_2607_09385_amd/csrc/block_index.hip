@@ -376,49 +376,78 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
   order[base[hist_at(bin, c, nch, top)] + rank] = item;
 }
 
-// Stable partition of the single-head work order into the XCD buckets
-// (one 1024-thread workgroup): thread t counts the buckets of a contiguous
-// chunk of the order, one exclusive scan over the bucket-major count table
-// gives every (bucket, thread) its output position, then each thread places
-// its items.  Within a bucket the items keep the heaviest-first order.
+// Stable partition of the single-head work order into the XCD buckets (one
+// 1024-thread workgroup).  The bucket of row r is (b*Hkv + g) % 8 =
+// (r / (nQB*G)) % 8.  A first pass counts each bucket (coalesced reads, wave
+// sums, LDS atomics) and writes the bucket starts; the second walks the order
+// in rounds of 1024 items, one per thread: per wave one ballot per bucket
+// gives each item its rank among the round's earlier items of its bucket, and
+// the per-wave counts, scanned over the waves, its round base.  Within a
+// bucket the items keep the heaviest-first order.
 __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
                                                  const int32_t* __restrict__ n_items,
                                                  int32_t* __restrict__ bucket) {
-  __shared__ int tab[kBuckets * 1024];
-  __shared__ int sh[32];
-  const int t = threadIdx.x;
+  __shared__ int base[kBuckets];           // bucket starts, then running bases
+  __shared__ int wpre[16][kBuckets];       // per-wave counts, then wave prefixes
+  __shared__ int round_tot[kBuckets];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = n_items[0];
-  const int per = (n + 1023) / 1024;
-  const int lo = min(t * per, n), hi = min(lo + per, n);
-  auto bucket_of = [&](int r) {
-    const int bh = r / p.nQB;
-    const int b = bh / p.Hq, h = bh - b * p.Hq;
-    return (b * p.Hkv + h / p.G) & (kBuckets - 1);
-  };
+  const int rows_per_g = p.nQB * p.G;
+  if (t < kBuckets) base[t] = 0;
+  __syncthreads();
   int c[kBuckets];
 #pragma unroll
   for (int k = 0; k < kBuckets; ++k) c[k] = 0;
-  for (int i = lo; i < hi; ++i) {
-    const int k = bucket_of(order[i]);
+  for (int i = t; i < n; i += 1024) {
+    const int k = (order[i] / rows_per_g) & (kBuckets - 1);
 #pragma unroll
     for (int kk = 0; kk < kBuckets; ++kk) c[kk] += kk == k;
   }
 #pragma unroll
-  for (int k = 0; k < kBuckets; ++k) tab[k * 1024 + t] = c[k];
+  for (int k = 0; k < kBuckets; ++k) {
+    int x = c[k];
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+    if (lane == 0 && x != 0) atomicAdd(&base[k], x);
+  }
   __syncthreads();
-  const int total = wg_scan_array(tab, kBuckets * 1024, sh);
-  if (t < kBuckets) bucket[t] = tab[t * 1024];
-  if (t == 0) bucket[kBuckets] = total;
-  int pos[kBuckets];
-#pragma unroll
-  for (int k = 0; k < kBuckets; ++k) pos[k] = tab[k * 1024 + t];
+  if (t == 0) {
+    int run = 0;
+    for (int k = 0; k < kBuckets; ++k) {
+      const int x = base[k];
+      base[k] = run;
+      bucket[k] = run;
+      run += x;
+    }
+    bucket[kBuckets] = run;
+  }
+  __syncthreads();
   int32_t* list = bucket + kBuckets + 1;
-  for (int i = lo; i < hi; ++i) {
-    const int item = order[i];
-    const int k = bucket_of(item);
+  for (int r0 = 0; r0 < n; r0 += 1024) {
+    const int i = r0 + t;
+    const int item = i < n ? order[i] : 0;
+    const int k = i < n ? (item / rows_per_g) & (kBuckets - 1) : -1;
+    unsigned long long mine = 0;
 #pragma unroll
-    for (int kk = 0; kk < kBuckets; ++kk)
-      if (kk == k) list[pos[kk]++] = item;
+    for (int kk = 0; kk < kBuckets; ++kk) {
+      const unsigned long long m = __ballot(k == kk);
+      if (lane == 0) wpre[wave][kk] = __popcll(m);
+      if (k == kk) mine = m;
+    }
+    __syncthreads();
+    if (t < kBuckets) {
+      int run = 0;
+      for (int w = 0; w < 16; ++w) {
+        const int x = wpre[w][t];
+        wpre[w][t] = run;
+        run += x;
+      }
+      round_tot[t] = run;
+    }
+    __syncthreads();
+    if (k >= 0) list[base[k] + wpre[wave][k] + __popcll(mine & ((1ull << lane) - 1))] = item;
+    __syncthreads();
+    if (t < kBuckets) base[t] += round_tot[t];
+    __syncthreads();
   }
 }
 
