@@ -310,25 +310,25 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
             msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
           }
         }
-        // P = 2^(S c - m), rounded to bf16 (the PV operand layout)
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt)
-#pragma unroll
-          for (int ch = 0; ch < 4; ++ch)
-#pragma unroll
-            for (int e = 0; e < 8; ++e)
-              pa[nt][ch][e] = (__bf16)__builtin_amdgcn_exp2f(
-                  __builtin_fmaf(sc[nt][ch >> 1][8 * (ch & 1) + e], a.c, -msafe[nt]));
-        // hand P and {alpha, m} to the O-wave of this head
+        // P = 2^(S c - m), rounded to bf16 (the PV operand layout), each
+        // 16-byte chunk handed to the O-wave as soon as it is computed, so
+        // the LDS writes run under the remaining exponentials
         {
           const int pb = g & 1;
+          *(f32x4*)((char*)smem + A_AT + (uint32_t)(pb * 4 + h) * 1024u + lane * 16) =
+              f32x4{alpha[0], alpha[1], m[0], m[1]};
           char* pdst = (char*)smem + P_AT + (uint32_t)(pb * 4 + h) * 8192u + lane * 16;
 #pragma unroll
           for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-            for (int ch = 0; ch < 4; ++ch) *(bf16x8*)(pdst + (nt * 4 + ch) * 1024) = pa[nt][ch];
-          *(f32x4*)((char*)smem + A_AT + (uint32_t)(pb * 4 + h) * 1024u + lane * 16) =
-              f32x4{alpha[0], alpha[1], m[0], m[1]};
+            for (int ch = 0; ch < 4; ++ch) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                pa[nt][ch][e] = (__bf16)__builtin_amdgcn_exp2f(
+                    __builtin_fmaf(sc[nt][ch >> 1][8 * (ch & 1) + e], a.c, -msafe[nt]));
+              *(bf16x8*)(pdst + (nt * 4 + ch) * 1024) = pa[nt][ch];
+              __builtin_amdgcn_sched_barrier(0);
+            }
         }
         lds_barrier();
         ++g;
