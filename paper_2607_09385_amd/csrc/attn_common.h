@@ -145,8 +145,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 template <int P> struct Par { static constexpr int value = P; };
 
 // Head packs of 4 at D = 128: two waves per head (scores and softmax; P V and
-// output), persistent (attn_ws.hip).
-hipError_t launch_attention_ws(const AttnArgs& a, hipStream_t s);
+// output), persistent (attn_ws.hip); prec: a Prec value.
+hipError_t launch_attention_ws(const AttnArgs& a, int prec, hipStream_t s);
 
 
 }  // namespace steel

@@ -663,8 +663,8 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
     ap.order = w.order_p;
     ap.n_items = w.n_items + 1;
     if (p.pack == 2) launch_one<D, 2, PREC>(ap, p.NP, s);
-    else if (D == 128 && PREC == kBf16 && (size_t)p.S_q * D * 4 < (1ull << 31))
-      launch_attention_ws(ap, s);
+    else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31))
+      launch_attention_ws(ap, PREC, s);
     else launch_one<D, 4, PREC>(ap, p.NP, s);
   }
   if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item

@@ -35,6 +35,13 @@
 // per head and buffer 64 lanes x {alpha[2], m[2]} (1 KiB).  Tile g's V is
 // copied during step g and read in step g + 1; tile g's K is copied two steps
 // ahead of its use.
+//
+// The fp8 forms (PREC, see internal.h) keep this schedule and change the
+// operands: V (and, with kFp8All, K) come as the pre-pass's E4M3 tiles (8
+// KiB, stored in their LDS layout, copied straight), the S-wave rounds P to
+// E4M3 (4 KiB per head and buffer) under an exact running maximum and keeps
+// the row sums itself (handed over with {alpha, m}), and both products run on
+// v_mfma_f32_32x32x64_f8f6f4 (Q quantized per row at each item's start).
 #include <utility>
 
 #include "attn_common.h"
@@ -77,6 +84,38 @@ __device__ __forceinline__ void ws_copy4(uint64_t base, uint32_t lds, uint32_t o
 }
 
 
+// Two 16-byte global -> LDS copies per lane (an 8 KiB E4M3 tile over the
+// four O-waves): copy j writes LDS bytes [lds + 1024 j + 16 lane, +16).
+__device__ __forceinline__ void ws_copy2(uint64_t base, uint32_t lds, uint32_t o0, uint32_t o1) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 4\n\t"
+      "global_load_lds_dwordx4 %2, %1\n\t"
+      "s_add_u32 m0, m0, 0x400\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %3, %1"
+      :
+      : "s"(lds), "s"(base), "v"(o0), "v"(o1)
+      : "memory", "m0", "scc");
+}
+
+typedef int i32x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f32x16 ws_mfma_e4m3(const i32x8& a, const i32x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+// 32 bytes of E4M3 operand from two 16-byte LDS reads.
+__device__ __forceinline__ i32x8 ws_lds_pair(const char* p0, const char* p1) {
+  const u32x4 lo = *(const u32x4*)p0, hi = *(const u32x4*)p1;
+  return __builtin_bit_cast(i32x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+__device__ __forceinline__ int ws_pack_e4m3(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(c, d, w, true);
+}
+
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
 // Workgroup barrier ordering LDS accesses only: the fences keep the compiler
@@ -93,19 +132,29 @@ __device__ __forceinline__ void lds_barrier() {
 
 // RAGGED: S_k is not a multiple of the block (the last key block's copies
 // clamp their rows); without it that path is compiled out.
-template <bool RAGGED, int GROUP>
+template <bool RAGGED, int GROUP, int PREC>
 __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
+  constexpr bool QK8 = PREC == kFp8All;  // S = K Q^T from E4M3 operands
+  constexpr bool PV8 = PREC != kBf16;    // O += V P from E4M3 operands
   constexpr int D = 128;
-  constexpr int C = D / 8;           // 16-byte chunks per row
-  constexpr int TB = kBlk * D * 2;   // bytes per K or V tile
-  constexpr int KS = D / 16;         // k-steps of S^T = K Q^T
+  constexpr int C = D / 8;           // 16-byte chunks per bf16 row
+  constexpr int TB = kBlk * D * 2;   // bytes per bf16 K or V tile
+  constexpr int TB8 = kBlk * D;      // bytes per E4M3 tile
+  constexpr int TBK = QK8 ? TB8 : TB, TBV = PV8 ? TB8 : TB;
+  constexpr int KCP = QK8 ? 2 : 4;   // copy instructions per lane of one K tile
+  constexpr int KS = D / 16;         // k-steps of S^T = K Q^T (bf16)
+  constexpr int KS8 = D / 64;        // k-steps of S^T = K Q^T (E4M3)
   constexpr int DT = D / 32;         // d tiles of O^T
-  constexpr float TAU = 8.0f;        // rescale only when a row max grows by > 2^8
+  // bf16 P: rescale only when a row max grows by > 2^8; E4M3 P: on every
+  // growth (its weights 2^(S - m + 8) need the exact maximum)
+  constexpr float TAU = PV8 ? 0.0f : 8.0f;
+  constexpr int PB = PV8 ? 4096 : 8192;  // P bytes per head and buffer
+  constexpr int AB = PV8 ? 2048 : 1024;  // {alpha, m} (and l) bytes per head and buffer
   constexpr uint32_t K_AT = 0;                 // K ring: 3 stages
-  constexpr uint32_t V_AT = 3 * TB;            // V ring: 2 stages
-  constexpr uint32_t P_AT = 5 * TB;            // P: [2 buffers][4 heads] x 8 KiB
-  constexpr uint32_t A_AT = P_AT + 8 * 8192;   // {alpha, m}: [2][4] x 1 KiB
-  constexpr uint32_t LDS_BYTES = A_AT + 8 * 1024;
+  constexpr uint32_t V_AT = 3 * TBK;           // V ring: 2 stages
+  constexpr uint32_t P_AT = V_AT + 2 * TBV;    // P: [2 buffers][4 heads]
+  constexpr uint32_t A_AT = P_AT + 8 * PB;     // {alpha, m (, l)}: [2][4]
+  constexpr uint32_t LDS_BYTES = A_AT + 8 * AB;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
   __shared__ __attribute__((aligned(1024))) char smem[LDS_BYTES];
 
@@ -172,6 +221,9 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
   auto load_entry_vec = [&](const Item& it, int base) __attribute__((always_inline)) -> uint32_t {
     return base + lane < it.L ? a.col[it.beg + base + lane] : 0u;
   };
+  auto kv_tile8 = [&](const Item& it) __attribute__((always_inline)) -> size_t {
+    return ((size_t)it.b * a.Hkv + it.h0 / a.G) * a.nKB;
+  };
   auto out_row_base = [&](const Item& it) __attribute__((always_inline)) -> size_t {
     return ((size_t)it.b * a.Hq + it.h0 + h) * a.S_q;  // row index of the head's row 0
   };
@@ -203,14 +255,56 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
     auto k_frag = [&](uint32_t kbase, int q) __attribute__((always_inline)) -> bf16x8 {  // q = 2*ks + sg
       return *(const bf16x8*)(lds_bytes + kbase + (q & 1) * 32 * D * 2 + koff[q >> 1]);
     };
-    bf16x8 qf[2][KS];
+    // E4M3 K fragment (sg, ks): row 32*sg + n, logical chunks 4*ks + 2*hf + {0, 1}
+    uint32_t koff8[QK8 ? KS8 : 1][2];
+#pragma unroll
+    for (int ks = 0; ks < (QK8 ? KS8 : 1); ++ks)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) koff8[ks][u] = (uint32_t)(n * D + 16 * ((4 * ks + 2 * hf + u) ^ kswz8<D>(n)));
+    auto k_frag8 = [&](uint32_t kbase, int sg, int ks) __attribute__((always_inline)) -> i32x8 {
+      const char* base = lds_bytes + kbase + sg * 32 * D;
+      return ws_lds_pair(base + koff8[ks][0], base + koff8[ks][1]);
+    };
+    // bf16: Q rows as the B operand (lane: row 32*nt + n, d = 16*ks + 8*hf + 0..7).
+    // E4M3: the raw rows (lane: d = 64*ks + 32*hf + 0..31) are quantized at
+    // the item's first step, with the row's own power-of-two scale.
+    bf16x8 qf[2][QK8 ? 8 : KS];
+    i32x8 q8[2][QK8 ? KS8 : 1];
+    float crow[2] = {a.c, a.c};  // per row: scores (MFMA units) to log2 units
     auto load_q = [&](const Item& it) __attribute__((always_inline)) {
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
         const int row = min(it.qb * kBlk + 32 * nt + n, a.S_q - 1);
-        const __bf16* qp = a.q + (((size_t)it.b * a.Hq + it.h0 + h) * a.S_q + row) * D + 8 * hf;
+        const __bf16* qr = a.q + (((size_t)it.b * a.Hq + it.h0 + h) * a.S_q + row) * D;
+        if constexpr (QK8) {
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qp + 16 * ks);
+          for (int u = 0; u < 8; ++u) qf[nt][u] = *(const bf16x8*)(qr + 64 * (u >> 2) + 32 * hf + 8 * (u & 3));
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) qf[nt][ks] = *(const bf16x8*)(qr + 8 * hf + 16 * ks);
+        }
+      }
+    };
+    auto quant_q = [&](const Item& it) __attribute__((always_inline)) {
+      const float dk = a.f8_scale[2 * ((size_t)it.b * a.Hkv + it.h0 / a.G)];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        float amax = 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) amax = fmaxf(amax, fabsf((float)qf[nt][u][e]));
+        const float sq = e4m3_scale(other_half_max(amax));
+#pragma unroll
+        for (int ks = 0; ks < KS8; ++ks)
+#pragma unroll
+          for (int w = 0; w < 8; ++w) {
+            const bf16x8& x = qf[nt][4 * ks + (w >> 1)];
+            const int e = 4 * (w & 1);
+            q8[nt][ks][w] = ws_pack_e4m3((float)x[e] * sq, (float)x[e + 1] * sq, (float)x[e + 2] * sq,
+                                         (float)x[e + 3] * sq);
+          }
+        crow[nt] = a.c / sq * dk;
       }
     };
     auto skip = [&](const Item&) __attribute__((always_inline)) {};
@@ -229,6 +323,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
     f32x16 sc[2][2];
     bf16x8 pa[2][4];
     float m[2] = {-INFINITY, -INFINITY};
+    float ls[2] = {0.f, 0.f};  // E4M3 P: the row sums, kept here
     int g = 0;     // step
     int ks3 = 0;   // g % 3: K stage
     while (have_x) {
@@ -242,14 +337,27 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
         }
         const int off = t - wbase;
         const uint32_t cw = (uint32_t)__builtin_amdgcn_readlane((int)(off < 64 ? win0 : win1), off & 63);
-        const uint32_t kbase = K_AT + (uint32_t)ks3 * TB;
+        const uint32_t kbase = K_AT + (uint32_t)ks3 * TBK;
         if (t == 0) {
           m[0] = -INFINITY;
           m[1] = -INFINITY;
+          ls[0] = 0.f;
+          ls[1] = 0.f;
+          if constexpr (QK8) quant_q(X);
         }
         // S^T = K Q^T: for each K fragment (keys 32 sg .. +31, k-step ks) the
         // two N-tiles; fragments read two ahead
-        {
+        if constexpr (QK8) {
+#pragma unroll
+          for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int ks = 0; ks < KS8; ++ks) {
+              const i32x8 kf = k_frag8(kbase, sg, ks);
+#pragma unroll
+              for (int nt = 0; nt < 2; ++nt)
+                sc[nt][sg] = ws_mfma_e4m3(kf, q8[nt][ks], ks == 0 ? f32x16{} : sc[nt][sg]);
+            }
+        } else {
           bf16x8 kf[3];
           kf[0] = k_frag(kbase, 0);
           kf[1] = k_frag(kbase, 1);
@@ -296,7 +404,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
 #pragma unroll
               for (int r = 0; r < 16; ++r) x = fmaxf(x, sc[nt][sg][r]);
             x = other_half_max(x);
-            mx[nt] = x == -INFINITY ? -INFINITY : x * a.c;
+            mx[nt] = x == -INFINITY ? -INFINITY : x * crow[nt];
             grow |= mx[nt] > m[nt] + TAU;
           }
           const bool any = __builtin_amdgcn_ballot_w64(grow) != 0;
@@ -306,10 +414,41 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
               const float mnew = fmaxf(m[nt], mx[nt]);
               alpha[nt] = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
               m[nt] = mnew;
+              if constexpr (PV8) ls[nt] *= alpha[nt];
             }
             msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
           }
         }
+        if constexpr (PV8) {
+          // P = 2^(S c - m + 8), at most 2^8 (m is the exact running
+          // maximum), rounded to E4M3 in the operand's byte order (byte
+          // 16*sg + r of the lane's 32 = register r of sub-tile sg); the row
+          // sums add the unrounded weights
+          const int pb = g & 1;
+          char* ad = (char*)smem + A_AT + (uint32_t)(pb * 4 + h) * AB + lane * 16;
+          *(f32x4*)ad = f32x4{alpha[0], alpha[1], m[0], m[1]};
+          char* pdst = (char*)smem + P_AT + (uint32_t)(pb * 4 + h) * PB + lane * 16;
+#pragma unroll
+          for (int nt = 0; nt < 2; ++nt) {
+            const float mo = 8.f - msafe[nt];
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg) {
+              float pv[16];
+#pragma unroll
+              for (int r = 0; r < 16; ++r)
+                pv[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[nt][sg][r], crow[nt], mo));
+#pragma unroll
+              for (int r = 0; r < 16; ++r) ls[nt] += pv[r];
+              const u32x4 w = {(uint32_t)ws_pack_e4m3(pv[0], pv[1], pv[2], pv[3]),
+                               (uint32_t)ws_pack_e4m3(pv[4], pv[5], pv[6], pv[7]),
+                               (uint32_t)ws_pack_e4m3(pv[8], pv[9], pv[10], pv[11]),
+                               (uint32_t)ws_pack_e4m3(pv[12], pv[13], pv[14], pv[15])};
+              *(u32x4*)(pdst + (nt * 2 + sg) * 1024) = w;
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+          *(f32x4*)(ad + 1024) = f32x4{ls[0], ls[1], 0.f, 0.f};
+        } else
         // P = 2^(S c - m), rounded to bf16 (the PV operand layout), each
         // 16-byte chunk handed to the O-wave as soon as it is computed, so
         // the LDS writes run under the remaining exponentials
@@ -377,6 +516,19 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
   auto kv_base = [&](const Item& it) __attribute__((always_inline)) -> size_t {
     return ((size_t)it.b * a.Hkv + it.h0 / a.G) * a.S_k * D;
   };
+  // E4M3 tile kb of an item's key/value head (stored as it sits in LDS, keys
+  // past S_k zero): two straight 16-byte pieces per lane
+  const uint32_t c8o0 = (uint32_t)(((ow * 2) * 64 + lane) * 16), c8o1 = (uint32_t)(((ow * 2 + 1) * 64 + lane) * 16);
+  auto issue_copy8 = [&](const uint8_t* src8, uint32_t dst, const Item& it, int kb) __attribute__((always_inline)) {
+    const uint64_t p = (uint64_t)(uintptr_t)(src8 + (kv_tile8(it) + (size_t)kb) * TB8);
+    const uint64_t ps = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(p >> 32)) << 32) |
+                        (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)p);
+    ws_copy2(ps, __builtin_amdgcn_readfirstlane(lds0 + dst + (uint32_t)(ow * 2) * 1024u), c8o0, c8o1);
+  };
+  auto copy_k = [&](uint32_t dst, const Item& it, int kb) __attribute__((always_inline)) {
+    if constexpr (QK8) issue_copy8(a.k8, dst, it, kb);
+    else issue_copy(a.k + kv_base(it), dst, kb);
+  };
   // V^T fragment (chunk, dt) of a V stage: the two transposed halves
   const int tg = lane >> 4, tr = (lane >> 2) & 3, tq = lane & 3;
   uint32_t voff[2][DT];
@@ -387,6 +539,15 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
       const int row = 8 * cc + 4 * (tg >> 1) + tr;
       voff[cc][dt] = (uint32_t)(tile_elem<D>(row, 4 * dt + 2 * (tg & 1) + (tq >> 1)) + 4 * (tq & 1)) * 2;
     }
+  // E4M3 V^T fragment dt: row 32*dt + n of the transposed tile, logical
+  // chunks 2*hf + {0, 1}
+  uint32_t voff8[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) voff8[u] = (uint32_t)(n * kBlk + 16 * ((2 * hf + u) ^ ((n >> 2) & 3)));
+  auto v_frag8 = [&](uint32_t vbase, int dt) __attribute__((always_inline)) -> i32x8 {
+    const char* base = lds_bytes + vbase + dt * 32 * kBlk;
+    return ws_lds_pair(base + voff8[0], base + voff8[1]);
+  };
   auto v_frag = [&](uint32_t vbase, int q) __attribute__((always_inline)) -> bf16x8 {  // q = 4*chunk + dt
     const int ch = q >> 2, dt = q & 3;
     const char* base = lds_bytes + vbase + (32 * (ch >> 1) + 16 * (ch & 1)) * D * 2;
@@ -401,13 +562,16 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
   float l[2] = {0.f, 0.f};
   auto write_rows = [&](const Item& it, const float* mz, bool zero) __attribute__((always_inline)) {
     const size_t rb = out_row_base(it);
+    // E4M3 forms: V's scale divided out here; the weights carry an extra 2^8
+    const float dvw = PV8 ? a.f8_scale[2 * ((size_t)it.b * a.Hkv + it.h0 / a.G) + 1] : 1.f;
+    constexpr float m_off = PV8 ? 8.f : 0.f;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const float lt = zero ? 0.f : half_pair_sum(l[t]);
-      const float inv = lt > 0.f ? 1.f / lt : 0.f;
+      const float inv = lt > 0.f ? dvw / lt : 0.f;
       const int row = it.qb * kBlk + 32 * t + n;
       if (a.lse != nullptr && hf == 0 && row < a.S_q)
-        a.lse[rb + row] = lt > 0.f ? (mz[t] + log2f(lt)) * 0.69314718055994531f : -INFINITY;
+        a.lse[rb + row] = lt > 0.f ? (mz[t] - m_off + log2f(lt)) * 0.69314718055994531f : -INFINITY;
       const size_t at = (rb + (size_t)min(row, a.S_q - 1)) * D + 4 * hf;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -466,7 +630,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
       int kb;
       bool in_y;
       if (!k_entry(p, kb, in_y)) break;
-      issue_copy(a.k + kv_base(in_y ? Y : X), K_AT + (uint32_t)p * TB, kb);
+      copy_k(K_AT + (uint32_t)p * TBK, in_y ? Y : X, kb);
       ++pk;
     }
   }
@@ -503,7 +667,50 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
           vf[q % 3], pa[nt][q >> 2], (FIRST && (q >> 2) == 0) ? f32x16{} : o[nt][q & 3], 0, 0, 0);
     });
   };
+  auto pv_mfmas8 = [&](uint32_t vbase, const i32x8 (&p8)[2], auto first_v) __attribute__((always_inline)) {
+    constexpr bool FIRST = decltype(first_v)::value != 0;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const i32x8 vf = v_frag8(vbase, dt);
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) o[nt][dt] = ws_mfma_e4m3(vf, p8[nt], FIRST ? f32x16{} : o[nt][dt]);
+    }
+  };
+  auto pv_step8 = [&](int gprev) __attribute__((always_inline)) {
+    const int pb = gprev & 1;
+    const char* ab = lds_bytes + A_AT + (uint32_t)(pb * 4 + h) * AB + lane * 16;
+    const f32x4 am = *(const f32x4*)ab;
+    i32x8 p8[2];
+    const char* psrc = lds_bytes + P_AT + (uint32_t)(pb * 4 + h) * PB + lane * 16;
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) p8[nt] = ws_lds_pair(psrc + (nt * 2) * 1024, psrc + (nt * 2 + 1) * 1024);
+    const uint32_t vbase = V_AT + (uint32_t)(gprev & 1) * TBV;
+    if (wu == 0) {
+      pv_mfmas8(vbase, p8, Par<1>{});
+    } else {
+      if (__builtin_amdgcn_ballot_w64(am[0] != 1.f || am[1] != 1.f) != 0) {
+        // O holds sums relative to the old maxima (the S-wave rescales l)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) o[t][dt] *= am[t];
+      }
+      pv_mfmas8(vbase, p8, Par<0>{});
+    }
+    mz[0] = am[2];
+    mz[1] = am[3];
+    if (wu == W.L - 1) {
+      const f32x4 al = *(const f32x4*)(ab + 1024);
+      l[0] = al[0];
+      l[1] = al[1];
+      write_rows(W, mz, false);
+    }
+  };
   auto pv_step = [&](int gprev) __attribute__((always_inline)) {
+    if constexpr (PV8) {
+      pv_step8(gprev);
+      return;
+    }
     const int pb = gprev & 1;
     const f32x4 am = *(const f32x4*)(lds_bytes + A_AT + (uint32_t)(pb * 4 + h) * 1024u + lane * 16);
     bf16x8 pa[2][4];
@@ -556,7 +763,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
       {
         const int off = t - wbase;
         const int kb = (int)(((uint32_t)__builtin_amdgcn_readlane((int)(off < 64 ? win0 : win1), off & 63)) & 0x7fffffffu);
-        issue_copy(a.v + kv_base(X), V_AT + (uint32_t)(g & 1) * TB, kb);
+        if constexpr (PV8) issue_copy8(a.v8, V_AT + (uint32_t)(g & 1) * TBV, X, kb);
+        else issue_copy(a.v + kv_base(X), V_AT + (uint32_t)(g & 1) * TB, kb);
       }
       // K tiles up to position t + 2 (two steps ahead; a position in the item
       // after Y is copied once that item is Y).  Before the barrier this
@@ -570,8 +778,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
         int kb;
         bool in_y;
         if (!k_entry(pk, kb, in_y)) break;
-        issue_copy(a.k + kv_base(in_y ? Y : X), K_AT + (uint32_t)kring * TB, kb);
-        kpend = pk == t + 2 ? 4 : 0;
+        copy_k(K_AT + (uint32_t)kring * TBK, in_y ? Y : X, kb);
+        kpend = pk == t + 2 ? KCP : 0;
         ++pk;
         kring = kring == 2 ? 0 : kring + 1;
       }
@@ -579,7 +787,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
       // this step's S tile becomes the O-wave's next tile
       if (t == 0) W = X;
       wu = t;
-      if (kpend == 4) wait_vm<4>();
+      if (kpend != 0) wait_vm<KCP>();
       else wait_vm<0>();
       lds_barrier();
       ++g;
@@ -600,16 +808,24 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
   if (wu >= 0) pv_step(g - 1);
 }
 
-hipError_t launch_attention_ws(const AttnArgs& a, hipStream_t s) {
+template <int PREC>
+static void launch_ws(const AttnArgs& a, hipStream_t s) {
   const long long np = (long long)a.R / 4;
   const bool few = np <= 4ll * 256;
-  if (a.S_k % kBlk != 0) {
-    if (few) hipLaunchKernelGGL((k_attn_ws<true, 4>), dim3(256), dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_ws<true, 16>), dim3(256), dim3(512), 0, s, a);
+  // E4M3 tiles are padded with zero keys: only bf16 K or V tiles clamp
+  if (PREC != kFp8All && a.S_k % kBlk != 0) {
+    if (few) hipLaunchKernelGGL((k_attn_ws<true, 4, PREC>), dim3(256), dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_ws<true, 16, PREC>), dim3(256), dim3(512), 0, s, a);
   } else {
-    if (few) hipLaunchKernelGGL((k_attn_ws<false, 4>), dim3(256), dim3(512), 0, s, a);
-    else hipLaunchKernelGGL((k_attn_ws<false, 16>), dim3(256), dim3(512), 0, s, a);
+    if (few) hipLaunchKernelGGL((k_attn_ws<false, 4, PREC>), dim3(256), dim3(512), 0, s, a);
+    else hipLaunchKernelGGL((k_attn_ws<false, 16, PREC>), dim3(256), dim3(512), 0, s, a);
   }
+}
+
+hipError_t launch_attention_ws(const AttnArgs& a, int prec, hipStream_t s) {
+  if (prec == kFp8All) launch_ws<kFp8All>(a, s);
+  else if (prec == kFp8Pv) launch_ws<kFp8Pv>(a, s);
+  else launch_ws<kBf16>(a, s);
   return hipGetLastError();
 }
 
