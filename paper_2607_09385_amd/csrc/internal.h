@@ -70,7 +70,7 @@ struct Fp8Buffers {
   float* part;   // [B*Hkv][kFp8Chunks][2]
   float* scale;  // [B*Hkv][2]
 };
-constexpr int kFp8Chunks = 32;
+constexpr int kFp8Chunks = 128;
 constexpr float kE4M3Max = 448.f;
 
 template <int D>

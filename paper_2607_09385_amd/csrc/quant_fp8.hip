@@ -45,15 +45,30 @@ __global__ __launch_bounds__(256) void k_fp8_amax(Problem p, const __bf16* __res
   const size_t base = ((size_t)bh * p.S_k + r0) * p.D;
   const int n8 = (r1 - r0) * p.D / 8;  // 16-byte groups
   float ak = 0.f, av = 0.f;
-  for (int i = threadIdx.x; i < n8; i += 256) {
-    const bf16x8 xv = *(const bf16x8*)(v + base + 8 * (size_t)i);
+  // four 16-byte loads in flight per thread and tensor
+  auto amax8 = [](float m, const bf16x8& x) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) av = fmaxf(av, fabsf((float)xv[e]));
+    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf((float)x[e]));
+    return m;
+  };
+  int i = threadIdx.x;
+  for (; i + 3 * 256 < n8; i += 4 * 256) {
+    bf16x8 xv[4], xk[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) xv[u] = *(const bf16x8*)(v + base + 8 * (size_t)(i + u * 256));
     if (with_k) {
-      const bf16x8 xk = *(const bf16x8*)(k + base + 8 * (size_t)i);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) ak = fmaxf(ak, fabsf((float)xk[e]));
+      for (int u = 0; u < 4; ++u) xk[u] = *(const bf16x8*)(k + base + 8 * (size_t)(i + u * 256));
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      av = amax8(av, xv[u]);
+      if (with_k) ak = amax8(ak, xk[u]);
+    }
+  }
+  for (; i < n8; i += 256) {
+    av = amax8(av, *(const bf16x8*)(v + base + 8 * (size_t)i));
+    if (with_k) ak = amax8(ak, *(const bf16x8*)(k + base + 8 * (size_t)i));
   }
   __shared__ float sh[2][4];
   ak = wave_max(ak);
@@ -76,11 +91,22 @@ __global__ __launch_bounds__(256) void k_fp8_tiles(Problem p, const __bf16* __re
                                                    const float* __restrict__ part, Fp8Buffers f) {
   constexpr int C = D / 16;  // 16-byte chunks per K8 row
   const int bh = (int)blockIdx.x / p.nKB, kb = (int)blockIdx.x % p.nKB;
+  // the head's maxima from its chunk partials (one per thread, then waves)
+  __shared__ float red[2][4];
   float ak = 0.f, av = 0.f;
-  for (int c = 0; c < kFp8Chunks; ++c) {
+  for (int c = threadIdx.x; c < kFp8Chunks; c += 256) {
     ak = fmaxf(ak, part[2 * (bh * kFp8Chunks + c)]);
     av = fmaxf(av, part[2 * (bh * kFp8Chunks + c) + 1]);
   }
+  ak = wave_max(ak);
+  av = wave_max(av);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = ak;
+    red[1][threadIdx.x >> 6] = av;
+  }
+  __syncthreads();
+  ak = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
+  av = fmaxf(fmaxf(red[1][0], red[1][1]), fmaxf(red[1][2], red[1][3]));
   const float sk = e4m3_scale(ak), sv = e4m3_scale(av);
   if (kb == 0 && threadIdx.x == 0) {
     f.scale[2 * bh] = 1.f / sk;
