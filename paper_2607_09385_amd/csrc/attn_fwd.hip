@@ -657,17 +657,21 @@ static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
 }
 
 template <int D, int PREC>
-static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStream_t s) {
+static hipError_t launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStream_t s) {
   if (p.pack > 1) {
     AttnArgs ap = a;
     ap.order = w.order_p;
     ap.n_items = w.n_items + 1;
-    if (p.pack == 2) launch_one<D, 2, PREC>(ap, p.NP, s);
-    else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31))
-      launch_attention_ws(ap, PREC, s);
-    else launch_one<D, 4, PREC>(ap, p.NP, s);
+    if (p.pack == 2) {
+      launch_one<D, 2, PREC>(ap, p.NP, s);
+    } else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31)) {
+      const hipError_t e = launch_attention_ws(ap, PREC, s);
+      if (e != hipSuccess) return e;
+    } else {
+      launch_one<D, 4, PREC>(ap, p.NP, s);
+    }
   }
-  if (p.pack > 1 && p.heads_share_mask) return;  // no single-head item
+  if (p.pack > 1 && p.heads_share_mask) return hipGetLastError();  // no single-head item
   a.order = w.order_s;
   a.n_items = w.n_items;
   a.bucket = w.bucket;
@@ -679,6 +683,7 @@ static void launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, hipStr
     grid = (int)(kBuckets * per);
   }
   launch_one<D, 1, PREC>(a, grid, s);
+  return hipGetLastError();
 }
 
 hipError_t launch_attention(const Problem& p, const void* q, const void* k, const void* v,
@@ -713,17 +718,9 @@ hipError_t launch_attention(const Problem& p, const void* q, const void* k, cons
   a.causal = p.causal;
   a.delta = p.delta;
   a.c = scale * 1.4426950408889634f;
-  if (p.fp8 == kFp8All) {
-    if (p.D == 64) launch_d<64, kFp8All>(p, a, w, s);
-    else launch_d<128, kFp8All>(p, a, w, s);
-  } else if (p.fp8 == kFp8Pv) {
-    if (p.D == 64) launch_d<64, kFp8Pv>(p, a, w, s);
-    else launch_d<128, kFp8Pv>(p, a, w, s);
-  } else {
-    if (p.D == 64) launch_d<64, kBf16>(p, a, w, s);
-    else launch_d<128, kBf16>(p, a, w, s);
-  }
-  return hipGetLastError();
+  if (p.fp8 == kFp8All) return p.D == 64 ? launch_d<64, kFp8All>(p, a, w, s) : launch_d<128, kFp8All>(p, a, w, s);
+  if (p.fp8 == kFp8Pv) return p.D == 64 ? launch_d<64, kFp8Pv>(p, a, w, s) : launch_d<128, kFp8Pv>(p, a, w, s);
+  return p.D == 64 ? launch_d<64, kBf16>(p, a, w, s) : launch_d<128, kBf16>(p, a, w, s);
 }
 
 }  // namespace steel
