@@ -42,12 +42,15 @@ typedef const __attribute__((address_space(4))) int32_t* cint_p;
 
 // The plan header (written by the index build) describes the same problem as
 // the kernel's arguments: every size, the causal limit and the head packing.
+// Every field is read unconditionally (no short circuit), so the compiler
+// fetches the header with one scalar load instead of one load per field.
 __device__ __forceinline__ bool plan_matches(const AttnArgs& a) {
   const cint_p h = (cint_p)a.header;
-  return h[kPfMagic] == kPlanMagic && h[kPfR] == a.R && h[kPfNKB] == a.nKB &&
-         h[kPfPack] == a.pack && h[kPfCausal] == a.causal && h[kPfDelta] == a.delta &&
-         h[kPfB] == a.B && h[kPfHq] == a.Hq && h[kPfHkv] == a.Hkv && h[kPfSq] == a.S_q &&
-         h[kPfSk] == a.S_k;
+  const bool ok = (h[kPfMagic] == kPlanMagic) & (h[kPfR] == a.R) & (h[kPfNKB] == a.nKB) &
+                  (h[kPfPack] == a.pack) & (h[kPfCausal] == a.causal) & (h[kPfDelta] == a.delta) &
+                  (h[kPfB] == a.B) & (h[kPfHq] == a.Hq) & (h[kPfHkv] == a.Hkv) & (h[kPfSq] == a.S_q) &
+                  (h[kPfSk] == a.S_k);
+  return ok;
 }
 
 __device__ __forceinline__ float other_half_max(float x) {

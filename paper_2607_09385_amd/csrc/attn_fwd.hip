@@ -174,17 +174,21 @@ __global__ __launch_bounds__((attn_threads<D, PACK, PREC>())) void k_attn(AttnAr
   __shared__ __attribute__((aligned(1024))) char smem[ST * SB];
 
   // index data is read-only during the kernel: scalar loads
-  if (!plan_matches(a)) return;  // index planned for another problem: out untouched
   int item;
   if (PACK == 1 && a.bucket != nullptr) {
     // single-head items: workgroup b runs on XCD b % 8 and takes the
-    // (b / 8)-th item of that XCD's bucket (heaviest first within it)
+    // (b / 8)-th item of that XCD's bucket (heaviest first within it).  The
+    // bucket bounds (always present) and the plan header are read together,
+    // so that the many workgroups past a short bucket leave after one load.
     const cint_p bk = (cint_p)a.bucket;
     const int x = (int)blockIdx.x & (kBuckets - 1), j = (int)blockIdx.x / kBuckets;
-    const int lo = bk[x];
-    if (j >= bk[x + 1] - lo) return;
+    const int lo = bk[x], hi = bk[x + 1];
+    const bool ok = plan_matches(a);
+    if (j >= hi - lo) return;
+    if (!ok) return;  // index planned for another problem: out untouched
     item = bk[kBuckets + 1 + lo + j];
   } else {
+    if (!plan_matches(a)) return;  // index planned for another problem: out untouched
     const int idx = xcd_slot((int)blockIdx.x);
     if (idx >= ((cint_p)a.n_items)[0]) return;
     item = ((cint_p)a.order)[idx];
