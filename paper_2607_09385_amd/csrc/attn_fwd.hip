@@ -187,6 +187,7 @@ __global__ __launch_bounds__((attn_threads<D, PACK, PREC>())) void k_attn(AttnAr
     if (j >= hi - lo) return;
     if (!ok) return;  // index planned for another problem: out untouched
     item = bk[kBuckets + 1 + lo + j];
+    if ((unsigned)item >= (unsigned)a.R) return;  // never for a well-formed index
   } else {
     if (!plan_matches(a)) return;  // index planned for another problem: out untouched
     const int idx = xcd_slot((int)blockIdx.x);

@@ -376,78 +376,112 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
   order[base[hist_at(bin, c, nch, top)] + rank] = item;
 }
 
-// Stable partition of the single-head work order into the XCD buckets (one
-// 1024-thread workgroup).  The bucket of row r is (b*Hkv + g) % 8 =
-// (r / (nQB*G)) % 8.  A first pass counts each bucket (coalesced reads, wave
-// sums, LDS atomics) and writes the bucket starts; the second walks the order
-// in rounds of 1024 items, one per thread: per wave one ballot per bucket
-// gives each item its rank among the round's earlier items of its bucket, and
-// the per-wave counts, scanned over the waves, its round base.  Within a
+// Stable partition of the single-head work order into the XCD buckets, one
+// 1024-thread workgroup per bucket.  The bucket of row r is
+// (b*Hkv + g) % 8 = (r / (nQB*G)) % 8.  Each workgroup takes the order in
+// slices of kSlice rounds of 1024 items (one per thread and round, the loads
+// of a slice issued together; a 12,288-item order is one slice, loaded once).
+// A first pass counts the items of lower buckets (this bucket's start) and of
+// its own.  Then, per slice: one ballot per round gives each wave's count of
+// own items, one wave scans the (round, wave) counts into bases, and every own
+// item goes to its base plus the count of its wave's earlier lanes.  Within a
 // bucket the items keep the heaviest-first order.
 __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
                                                  const int32_t* __restrict__ n_items,
                                                  int32_t* __restrict__ bucket) {
-  __shared__ int base[kBuckets];           // bucket starts, then running bases
-  __shared__ int wpre[16][kBuckets];       // per-wave counts, then wave prefixes
-  __shared__ int round_tot[kBuckets];
+  constexpr int kSlice = 16;               // rounds of 1024 items per slice
+  __shared__ int tab[kSlice * 16];         // (round, wave) counts, then bases
+  __shared__ int red[2][16];
+  __shared__ int slice_total;
+  const int mb = (int)blockIdx.x;  // this workgroup's bucket
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = n_items[0];
   const int rows_per_g = p.nQB * p.G;
-  if (t < kBuckets) base[t] = 0;
-  __syncthreads();
-  int c[kBuckets];
+  // r / rows_per_g without an integer division (a long instruction sequence
+  // per item): the double quotient is within one of the truth for r < 2^31,
+  // and one correction step makes it exact
+  const double inv_g = 1.0 / (double)rows_per_g;
+  auto bucket_of = [&](int it) {
+    int q = (int)((double)it * inv_g);
+    const int rem = it - q * rows_per_g;
+    q += (rem >= rows_per_g) - (rem < 0);
+    return it < 0 ? -1 : q & (kBuckets - 1);
+  };
+  int item[kSlice], kr[kSlice];
+  auto load = [&](int s0) {
 #pragma unroll
-  for (int k = 0; k < kBuckets; ++k) c[k] = 0;
-  for (int i = t; i < n; i += 1024) {
-    const int k = (order[i] / rows_per_g) & (kBuckets - 1);
+    for (int r = 0; r < kSlice; ++r) {
+      const int i = s0 + 1024 * r + t;
+      item[r] = i < n ? order[i] : -1;
+    }
 #pragma unroll
-    for (int kk = 0; kk < kBuckets; ++kk) c[kk] += kk == k;
+    for (int r = 0; r < kSlice; ++r) kr[r] = bucket_of(item[r]);
+  };
+  const bool one = n <= kSlice * 1024;  // the whole order stays in registers
+  // pass 1: items of lower buckets and of this one
+  int below = 0, own = 0;
+  for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
+    load(s0);
+#pragma unroll
+    for (int r = 0; r < kSlice; ++r) {
+      below += kr[r] >= 0 && kr[r] < mb;
+      own += kr[r] == mb;
+    }
   }
-#pragma unroll
-  for (int k = 0; k < kBuckets; ++k) {
-    int x = c[k];
-    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
-    if (lane == 0 && x != 0) atomicAdd(&base[k], x);
+  for (int off = 32; off > 0; off >>= 1) {
+    below += __shfl_xor(below, off);
+    own += __shfl_xor(own, off);
+  }
+  if (lane == 0) {
+    red[0][wave] = below;
+    red[1][wave] = own;
   }
   __syncthreads();
+  int run = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    run += red[0][w];
+    total += red[1][w];
+  }
   if (t == 0) {
-    int run = 0;
-    for (int k = 0; k < kBuckets; ++k) {
-      const int x = base[k];
-      base[k] = run;
-      bucket[k] = run;
-      run += x;
-    }
-    bucket[kBuckets] = run;
+    bucket[mb] = run;
+    if (mb == kBuckets - 1) bucket[kBuckets] = run + total;
   }
-  __syncthreads();
+  // pass 2: this bucket's items in order, one slice at a time
   int32_t* list = bucket + kBuckets + 1;
-  for (int r0 = 0; r0 < n; r0 += 1024) {
-    const int i = r0 + t;
-    const int item = i < n ? order[i] : 0;
-    const int k = i < n ? (item / rows_per_g) & (kBuckets - 1) : -1;
-    unsigned long long mine = 0;
+  for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
+    if (!one) load(s0);
 #pragma unroll
-    for (int kk = 0; kk < kBuckets; ++kk) {
-      const unsigned long long m = __ballot(k == kk);
-      if (lane == 0) wpre[wave][kk] = __popcll(m);
-      if (k == kk) mine = m;
+    for (int r = 0; r < kSlice; ++r) {
+      const unsigned long long m = __ballot(kr[r] == mb);
+      if (lane == 0) tab[r * 16 + wave] = __popcll(m);
     }
     __syncthreads();
-    if (t < kBuckets) {
-      int run = 0;
-      for (int w = 0; w < 16; ++w) {
-        const int x = wpre[w][t];
-        wpre[w][t] = run;
-        run += x;
+    if (wave == 0) {  // exclusive scan of the 256 counts in (round, wave) order
+      int v[4], sum = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        v[j] = sum;
+        sum += tab[4 * lane + j];
       }
-      round_tot[t] = run;
+      int incl = sum;  // inclusive scan of the lane sums
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (lane >= off) incl += y;
+      }
+      const int excl = run + incl - sum;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tab[4 * lane + j] = excl + v[j];
+      if (lane == 63) slice_total = incl;
     }
     __syncthreads();
-    if (k >= 0) list[base[k] + wpre[wave][k] + __popcll(mine & ((1ull << lane) - 1))] = item;
-    __syncthreads();
-    if (t < kBuckets) base[t] += round_tot[t];
-    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kSlice; ++r) {
+      const bool sel = kr[r] == mb;
+      const unsigned long long m = __ballot(sel);
+      if (sel) list[tab[r * 16 + wave] + __popcll(m & ((1ull << lane) - 1))] = item[r];
+    }
+    run += slice_total;
+    __syncthreads();  // tab and slice_total are rewritten by the next slice
   }
 }
 
@@ -472,7 +506,7 @@ hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const Index
                      wide, w.cnt, w.row_ptr, w.col, w.hist_s, w.hist_p, w.n_items, w.order_s,
                      w.order_p, rows_grid, nch_s);
   if (w.bucket != nullptr)
-    hipLaunchKernelGGL(k_bucket, dim3(1), dim3(1024), 0, s, p, w.order_s, w.n_items, w.bucket);
+    hipLaunchKernelGGL(k_bucket, dim3(kBuckets), dim3(1024), 0, s, p, w.order_s, w.n_items, w.bucket);
   return hipGetLastError();
 }
 
