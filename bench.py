@@ -88,21 +88,32 @@ def traffic_for(workload):
     return entry.get("bytes_per_run")
 
 
-# Softmax work per element of a live tile, in VALU cycles of one SIMD for a
-# 64-lane instruction: exp2 (a transcendental, quarter rate: 16 cycles), the
-# fma that forms its argument (4), half a 3-input max (2), half a packed bf16
-# conversion (2), half a bf16 dot2 for the row sum (2): 26 cycles per 64
-# elements.
-VALU_CYCLES_PER_ELEM = (16 + 4 + 2 + 2 + 2) / 64.0
+# Softmax work per element of a live tile: one exp2, the fma that forms its
+# argument, and half each of a 3-input max, a packed bf16 conversion and a bf16
+# dot2 for the row sum.  Cycles per 64-lane instruction measured by
+# `bench.py --mfma-peak` (steel_valu_rate, shader clock): a SIMD with eight
+# resident waves sustains v_exp_f32 every 2.6 cycles and v_fma_f32 every 1.56,
+# while a single wave issues them only every 14.5 and 9.0 cycles (the other
+# three instructions are taken at the fma's rate).
+VALU_CYCLES_SIMD = 2.6 + 1.56 + 1.5 * 1.56        # per 64 elements, SIMD throughput
+VALU_CYCLES_ONE_WAVE = 14.5 + 9.0 + 1.5 * 9.0     # per 64 elements, issued by one wave
 
 
 def valu_bound(n_live, D):
-    """Time the softmax alone would take on all 1,024 SIMDs at 2.4 GHz: the
-    plain-ALU bound beside the MFMA one."""
-    cycles = n_live * 64 * 64 * VALU_CYCLES_PER_ELEM
-    us = cycles / (256 * 4 * 2.4e9) * 1e6
+    """The softmax alone on all 1,024 SIMDs at 2.4 GHz: at the SIMD's VALU
+    throughput (the plain-ALU bound beside the MFMA one), and issued by one
+    wave per SIMD at the single-wave rate together with that wave's own score
+    MFMAs, which hold its issue (the structure of the wave-specialised kernel,
+    whose one S-wave per head computes the scores and the softmax of 64 rows)."""
+    elems = n_live * 64 * 64
+    us = elems * VALU_CYCLES_SIMD / 64 / (256 * 4 * 2.4e9) * 1e6
+    one = (elems * VALU_CYCLES_ONE_WAVE / 64 + n_live * (D // 4) * 32) / (256 * 4 * 2.4e9) * 1e6
     return {"bound": "alu", "us": round(us, 1),
-            "model": "per live element: exp2 (quarter rate) + fma + half max3 + half cvt_pk_bf16 + half dot2, 64 lanes per 4 cycles",
+            "model": "per live element: exp2 + fma + half max3 + half cvt_pk_bf16 + half dot2 at the measured "
+                     "SIMD rates (v_exp_f32 2.6, v_fma_f32 1.56 cycles per 64 lanes)",
+            "one_wave_softmax_us": round(one, 1),
+            "one_wave_model": "same instructions issued by one wave per SIMD (v_exp_f32 every 14.5, others every "
+                              "9.0 cycles) plus that wave's D/4 score MFMAs per tile (32 cycles each)",
             "mfma_us_at_peak": round(4.0 * 64 * 64 * D * n_live / PEAK_TFLOPS / 1e6, 1)}
 
 
@@ -207,7 +218,38 @@ def mfma_peak(iters=400000, waves_per_wg=4):
         ghz = float((c[:, 0] / (c[:, 1] / 100e6)).mean() / 1e9)
         res[kind] = {"tflops": round(flops / t / 1e12, 1), "frac_of_peak": round(flops / t / 1e12 / PEAK_TFLOPS, 3),
                      "ms": round(t * 1e3, 2), "avg_clock_ghz": round(ghz, 3)}
+    res["valu"] = {name: [valu_rate(op, waves_per_wg=w, grid=g)
+                          for w, g in ((4, 256), (8, 256), (16, 256), (16, 512))]
+                   for op, name in ((0, "v_exp_f32"), (1, "v_fma_f32"))}
     return res
+
+
+def valu_rate(op, iters=200000, waves_per_wg=16, grid=256):
+    """Cycles per 64-lane instruction on one SIMD (steel_valu_rate: eight
+    independent chains of v_exp_f32 (op 0) or v_fma_f32 (op 1) per lane, grid *
+    waves_per_wg / 1024 waves per SIMD, all resident at once), from the
+    kernel's own shader-clock cycles, so independent of the clock.  With one
+    wave per SIMD it is the issue interval of a single wave; with several, the
+    SIMD's throughput."""
+    import torch
+    from paper_2607_09385_amd import _lib
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    seed = torch.linspace(-1.0, 1.0, 8, dtype=torch.float32, device=dev)
+    sink = torch.empty(grid * 64 * waves_per_wg, dtype=torch.float32, device=dev)
+    clocks = torch.zeros(2 * grid, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    for n in (iters // 4, iters):
+        st = lib.steel_valu_rate(op, seed.data_ptr(), n, grid, waves_per_wg, sink.data_ptr(),
+                                 clocks.data_ptr(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"steel_valu_rate failed ({st})")
+    torch.cuda.synchronize()
+    c = clocks.view(grid, 2).cpu().double()
+    waves_per_simd = grid * waves_per_wg / 1024
+    per_instr = float(c[:, 0].mean()) / (iters * 8 * waves_per_simd)
+    return {"waves_per_simd": waves_per_simd, "cycles_per_wave_instruction": round(per_instr, 2),
+            "finite": bool(torch.isfinite(sink).all().item())}
 
 
 COPY_BYTES = 256 << 20   # reference elementwise kernel for the counter scale

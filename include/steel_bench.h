@@ -1,11 +1,12 @@
 /*
- * libsteel measurement helper (not part of the attention path): the
+ * libsteel measurement helpers (not part of the attention path): the
  * achievable rate of the bf16 matrix-core instruction the attention kernels
  * use (v_mfma_f32_32x32x16_bf16), as the context for their roofline
- * fraction.  The paper measures against its device's peak (Section V-A);
- * here the published peak (256 CU x 2.4 GHz x 4096 bf16 flop/clk/CU) is the
- * denominator, and this rate shows what the chip sustains under the matrix
- * cores' power draw for given operand data.
+ * fraction, and the issue rates of the softmax's exponential and fma
+ * (v_exp_f32, v_fma_f32), the basis of the plain-ALU estimate.  The paper measures against its device's
+ * peak (Section V-A); here the published peak (256 CU x 2.4 GHz x 4096 bf16
+ * flop/clk/CU) is the denominator, and the matrix-core rate shows what the
+ * chip sustains under the matrix cores' power draw for given operand data.
  */
 #ifndef STEEL_BENCH_H
 #define STEEL_BENCH_H
@@ -32,6 +33,25 @@ extern "C" {
  * a launch error.  Timing is the caller's (events around the call).
  */
 int steel_mfma_peak(const void* operands, int iters, int grid, int waves_per_wg, float* sink,
+                    unsigned long long* clocks, void* stream);
+
+/*
+ * Enqueue grid workgroups of waves_per_wg waves; every lane runs iters
+ * iterations over eight independent floats of one VALU instruction of the
+ * online softmax (Algorithm 1, second stage): op 0 x <- 2^(-x) (eight
+ * v_exp_f32 per iteration, the negation folded into the instruction), op 1
+ * x <- x * 0.999 + 0.0001 (eight v_fma_f32).
+ *
+ *   seed    device float [8]: the starting values (any finite values)
+ *   sink    device float [grid * 64 * waves_per_wg], as for steel_mfma_peak
+ *   clocks  device uint64 [2 * grid], as for steel_mfma_peak: shader-clock
+ *           cycles over the loop give the cycles per 64-lane instruction
+ *   stream  hipStream_t as void*, or NULL
+ *
+ * Returns 0 when enqueued, 1 on an invalid argument (nothing enqueued), 3 on
+ * a launch error.
+ */
+int steel_valu_rate(int op, const float* seed, int iters, int grid, int waves_per_wg, float* sink,
                     unsigned long long* clocks, void* stream);
 
 #ifdef __cplusplus
