@@ -143,9 +143,11 @@ __device__ int wg_exclusive_scan(int x, int* sh, int& total) {
 }
 
 // In-place exclusive scan of a[0 .. n) (LDS or global) by a 1024-thread
-// workgroup, contiguous segments per thread; returns the total.
+// workgroup, contiguous segments per thread; returns the total.  The segment
+// length is odd, so the 64 lanes of a wave walking their segments in step hit
+// 64 different LDS banks (an even length put up to 8 lanes on one bank).
 __device__ int wg_scan_array(int* a, long long n, int* sh) {
-  const long long per = (n + 1023) / 1024;
+  const long long per = ((n + 1023) / 1024) | 1;
   const long long lo = min((long long)threadIdx.x * per, n), hi = min(lo + per, n);
   int s = 0;
   for (long long i = lo; i < hi; ++i) s += a[i];
@@ -235,7 +237,7 @@ __global__ __launch_bounds__(1024) void k_scan_small(Problem p, const int32_t* _
           c = cnt[bh * p.pack * p.nQB + qb];
           present = (c & (int)kUniformBit) != 0;
         }
-        if (present) fn(i, count_bin(c & ~(int)kUniformBit));
+        fn(i, present ? count_bin(c & ~(int)kUniformBit) : -1);  // -1: not in this list
         qb += dr;
         bh += dq;
         if (qb >= p.nQB) {
@@ -262,7 +264,18 @@ __global__ __launch_bounds__(1024) void k_scan_small(Problem p, const int32_t* _
     const int E = (top + 1) * nch;
     for (int i = t; i < E; i += 1024) hist[i] = 0;
     __syncthreads();
-    walk([&](int i, int bin) { atomicAdd(&hist[hist_at(bin, i / kChunk, nch, top)], 1); });
+    // a wave's 64 items fall in one chunk; when they also share one bin (a
+    // uniform mask) one lane adds the wave's count, else each lane adds one
+    walk([&](int i, int bin) {
+      const int at = bin >= 0 ? hist_at(bin, i / kChunk, nch, top) : -1;
+      const int a0 = __builtin_amdgcn_readfirstlane(at);
+      const unsigned long long act = __ballot(true);
+      if (__ballot(at == a0) == act) {
+        if (a0 >= 0 && (t & 63) == __builtin_ctzll(act)) atomicAdd(&hist[a0], __popcll(act));
+      } else if (at >= 0) {
+        atomicAdd(&hist[at], 1);
+      }
+    });
     __syncthreads();
     const int n = wg_scan_array(hist, E, sh);
     int32_t* g = list == 0 ? hist_s : hist_p;
