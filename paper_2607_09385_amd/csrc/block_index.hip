@@ -264,16 +264,20 @@ __global__ __launch_bounds__(1024) void k_scan_small(Problem p, const int32_t* _
     const int E = (top + 1) * nch;
     for (int i = t; i < E; i += 1024) hist[i] = 0;
     __syncthreads();
-    // a wave's 64 items fall in one chunk; when they also share one bin (a
-    // uniform mask) one lane adds the wave's count, else each lane adds one
+    // a wave's 64 items are consecutive rows in one chunk, whose bins come in
+    // runs: the first lane of each run of equal entries adds the run's length
+    // (the active lanes are a prefix of the wave)
     walk([&](int i, int bin) {
       const int at = bin >= 0 ? hist_at(bin, i / kChunk, nch, top) : -1;
-      const int a0 = __builtin_amdgcn_readfirstlane(at);
+      const int ln = t & 63;
+      const int prev = __shfl_up(at, 1);
       const unsigned long long act = __ballot(true);
-      if (__ballot(at == a0) == act) {
-        if (a0 >= 0 && (t & 63) == __builtin_ctzll(act)) atomicAdd(&hist[a0], __popcll(act));
-      } else if (at >= 0) {
-        atomicAdd(&hist[at], 1);
+      const bool first = ln == 0 || prev != at;
+      const unsigned long long starts = __ballot(first);
+      if (first && at >= 0) {
+        const unsigned long long above = ln == 63 ? 0ull : starts & (~0ull << (ln + 1));
+        const int end = above != 0 ? __builtin_ctzll(above) : 64 - __builtin_clzll(act);
+        atomicAdd(&hist[at], end - ln);
       }
     });
     __syncthreads();
