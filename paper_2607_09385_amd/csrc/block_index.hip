@@ -348,15 +348,18 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
     int pos = row_ptr[r];
     for (int kb0 = 4 * lane; kb0 - 4 * lane < p.nKB; kb0 += 256) {
       const uint32_t bits = kb0 < p.nKB ? live_quad(p, mrow, wide, qb, kb0) : 0u;
-      // this 256-block's entries in kb order: lane-major, 4 per lane
-      const int mine = __popc(bits);
-      int before = mine;
-      for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(before, off);
-        if (lane >= off) before += y;
+      // this 256-block's entries in kb order: lane-major, 4 per lane; the
+      // entries of earlier lanes counted per bit position (one ballot and
+      // one masked bit count each)
+      int before = 0, total = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const unsigned long long m = __ballot((bits >> e) & 1u);
+        before += (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        total += __popcll(m);
       }
-      const int total = __shfl(before, 63);
-      int k = pos + before - mine;
+      int k = pos + before;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
         if ((bits >> e) & 1u) {
