@@ -725,9 +725,9 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, "
-              f"WORLD_SIZE={world}); the path shards by head/group with no exchange, "
-              "which is described but not run here", file=sys.stderr)
+        print(f"bench.py: measures one GPU only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}); the path would shard by key/value group with no "
+              "exchange between GPUs, which is not implemented", file=sys.stderr)
         sys.exit(2)
     if args.traffic_run:
         traffic_run(args.workload, args.steps if args.steps != 50 else 5)
