@@ -47,7 +47,7 @@ PEAK_TFLOPS = 256 * 2.4e9 * 4096 / 1e12     # 2516.6
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2607_09385_amd", "csrc", f)
-               for f in ("attn_common.h", "attn_fwd.hip", "attn_ws.hip")]
+               for f in ("attn_common.h", "attn_fwd.hip", "attn_ws.hip", "block_index.hip")]
 
 
 def live_tile_counts(mask, B, Hq, S_q, S_k, causal, blk=64):
@@ -65,8 +65,9 @@ def live_tile_counts(mask, B, Hq, S_q, S_k, causal, blk=64):
 
 
 def kernel_hash():
-    """Hash of the attention kernels' sources: counter readings taken on other
-    sources are not reported."""
+    """Hash of the attention kernels' sources and of the index build (whose
+    work order sets which tiles each XCD's L2 sees together): counter readings
+    taken on other sources are not reported."""
     h = hashlib.sha256()
     for path in KERNEL_SRCS:
         with open(path, "rb") as f:

@@ -397,36 +397,52 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
 }
 
 // Stable partition of the single-head work order into the XCD buckets, one
-// 1024-thread workgroup per bucket.  The bucket of row r is
-// (b*Hkv + g) % 8 = (r / (nQB*G)) % 8.  Each workgroup takes the order in
-// slices of kSlice rounds of 1024 items (one per thread and round, the loads
-// of a slice issued together; a 12,288-item order is one slice, loaded once).
-// A first pass counts the items of lower buckets (this bucket's start) and of
-// its own.  Then, per slice: one ballot per round gives each wave's count of
-// own items, one wave scans the (round, wave) counts into bases, and every own
-// item goes to its base plus the count of its wave's earlier lanes.  Within a
-// bucket the items keep the heaviest-first order.
+// 1024-thread workgroup per bucket.  The bucket of row r is g % 8, with
+// g = r / (nQB*G) = b*Hkv + (key/value head).  Within a bucket the items go
+// head by head: the bucket's heads g = mb, mb + 8, ... fall into at most kKeys
+// consecutive ranges (one head per range when a bucket holds at most kKeys
+// heads), the ranges in increasing g, and within a range the items keep the
+// heaviest-first order.  The workgroups an XCD runs at one time then read the
+// key/value tiles of one head, which its L2 keeps, instead of those of all
+// the bucket's heads.
+// Each workgroup takes the order in slices of kSlice rounds of 1024 items
+// (one per thread and round, the loads of a slice issued together; a
+// 12,288-item order is one slice, loaded once).  A first pass counts the
+// items of lower buckets (this bucket's start) and this bucket's items per
+// range.  Then, per slice and range: one ballot per round gives each wave's
+// count, one wave per range scans its (round, wave) counts into bases, and
+// every item goes to its base plus the count of its wave's earlier lanes.
 __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
                                                  const int32_t* __restrict__ n_items,
                                                  int32_t* __restrict__ bucket) {
-  constexpr int kSlice = 16;               // rounds of 1024 items per slice
-  __shared__ int tab[kSlice * 16];         // (round, wave) counts, then bases
-  __shared__ int red[2][16];
-  __shared__ int slice_total;
+  constexpr int kSlice = 16;                // rounds of 1024 items per slice
+  constexpr int kKeys = 8;                  // head ranges per bucket, at most
+  __shared__ int tab[kKeys * kSlice * 16];  // (range, round, wave) counts, then bases
+  __shared__ int red[16];
+  __shared__ int key_n[kKeys];     // this bucket's items per range
+  __shared__ int key_base[kKeys];  // list position of the range's next item
   const int mb = (int)blockIdx.x;  // this workgroup's bucket
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = n_items[0];
   const int rows_per_g = p.nQB * p.G;
+  const int heads = p.B * p.Hkv;
+  const int nsub = (heads + kBuckets - 1) / kBuckets;  // heads of a bucket, at most
+  const int nkey = nsub < kKeys ? nsub : kKeys;
+  const int per = (nsub + nkey - 1) / nkey;  // heads per range
   // r / rows_per_g without an integer division (a long instruction sequence
   // per item): the double quotient is within one of the truth for r < 2^31,
   // and one correction step makes it exact
   const double inv_g = 1.0 / (double)rows_per_g;
-  auto bucket_of = [&](int it) {
+  auto group_of = [&](int it) {
     int q = (int)((double)it * inv_g);
     const int rem = it - q * rows_per_g;
     q += (rem >= rows_per_g) - (rem < 0);
-    return it < 0 ? -1 : q & (kBuckets - 1);
+    return q;
   };
+  if (t < kKeys) key_n[t] = 0;
+  __syncthreads();
+  // item[r]: the order entry of round r; kr[r]: its head range when it is in
+  // this bucket, else -1.  Returns the thread's count of lower-bucket items.
   int item[kSlice], kr[kSlice];
   auto load = [&](int s0) {
 #pragma unroll
@@ -434,74 +450,88 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
       const int i = s0 + 1024 * r + t;
       item[r] = i < n ? order[i] : -1;
     }
-#pragma unroll
-    for (int r = 0; r < kSlice; ++r) kr[r] = bucket_of(item[r]);
-  };
-  const bool one = n <= kSlice * 1024;  // the whole order stays in registers
-  // pass 1: items of lower buckets and of this one
-  int below = 0, own = 0;
-  for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
-    load(s0);
+    int below = 0;
 #pragma unroll
     for (int r = 0; r < kSlice; ++r) {
-      below += kr[r] >= 0 && kr[r] < mb;
-      own += kr[r] == mb;
+      const int g = item[r] < 0 ? -1 : group_of(item[r]);
+      const int bk = g & (kBuckets - 1);
+      below += g >= 0 && bk < mb;
+      const int sub = g / kBuckets;
+      kr[r] = g >= 0 && bk == mb ? (per == 1 ? sub : sub / per) : -1;
+    }
+    return below;
+  };
+  const bool one = n <= kSlice * 1024;  // the whole order stays in registers
+  // pass 1: items of lower buckets, and of this one per range
+  int below = 0;
+  for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
+    below += load(s0);
+#pragma unroll 1
+    for (int k = 0; k < nkey; ++k) {
+      int c = 0;
+#pragma unroll
+      for (int r = 0; r < kSlice; ++r) c += __popcll(__ballot(kr[r] == k));
+      if (lane == 0 && c) atomicAdd(&key_n[k], c);
     }
   }
-  for (int off = 32; off > 0; off >>= 1) {
-    below += __shfl_xor(below, off);
-    own += __shfl_xor(own, off);
-  }
-  if (lane == 0) {
-    red[0][wave] = below;
-    red[1][wave] = own;
+  for (int off = 32; off > 0; off >>= 1) below += __shfl_xor(below, off);
+  if (lane == 0) red[wave] = below;
+  __syncthreads();
+  if (t == 0) {
+    int run = 0;
+    for (int w = 0; w < 16; ++w) run += red[w];
+    bucket[mb] = run;
+    for (int k = 0; k < nkey; ++k) {
+      key_base[k] = run;
+      run += key_n[k];
+    }
+    if (mb == kBuckets - 1) bucket[kBuckets] = run;
   }
   __syncthreads();
-  int run = 0, total = 0;
-  for (int w = 0; w < 16; ++w) {
-    run += red[0][w];
-    total += red[1][w];
-  }
-  if (t == 0) {
-    bucket[mb] = run;
-    if (mb == kBuckets - 1) bucket[kBuckets] = run + total;
-  }
-  // pass 2: this bucket's items in order, one slice at a time
+  // pass 2: this bucket's items in range order, one slice at a time
   int32_t* list = bucket + kBuckets + 1;
   for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
     if (!one) load(s0);
+#pragma unroll 1
+    for (int k = 0; k < nkey; ++k) {
 #pragma unroll
-    for (int r = 0; r < kSlice; ++r) {
-      const unsigned long long m = __ballot(kr[r] == mb);
-      if (lane == 0) tab[r * 16 + wave] = __popcll(m);
+      for (int r = 0; r < kSlice; ++r) {
+        const unsigned long long m = __ballot(kr[r] == k);
+        if (lane == 0) tab[(k * kSlice + r) * 16 + wave] = __popcll(m);
+      }
     }
     __syncthreads();
-    if (wave == 0) {  // exclusive scan of the 256 counts in (round, wave) order
+    if (wave < nkey) {  // wave k: exclusive scan of range k's 256 (round, wave) counts
+      int* tk = tab + wave * kSlice * 16;
       int v[4], sum = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         v[j] = sum;
-        sum += tab[4 * lane + j];
+        sum += tk[4 * lane + j];
       }
       int incl = sum;  // inclusive scan of the lane sums
       for (int off = 1; off < 64; off <<= 1) {
         const int y = __shfl_up(incl, off);
         if (lane >= off) incl += y;
       }
-      const int excl = run + incl - sum;
+      const int base = key_base[wave];
+      const int excl = base + incl - sum;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) tab[4 * lane + j] = excl + v[j];
-      if (lane == 63) slice_total = incl;
+      for (int j = 0; j < 4; ++j) tk[4 * lane + j] = excl + v[j];
+      const int slice_n = __shfl(incl, 63);
+      if (lane == 0) key_base[wave] = base + slice_n;  // only this wave touches it
     }
     __syncthreads();
+#pragma unroll 1
+    for (int k = 0; k < nkey; ++k) {
 #pragma unroll
-    for (int r = 0; r < kSlice; ++r) {
-      const bool sel = kr[r] == mb;
-      const unsigned long long m = __ballot(sel);
-      if (sel) list[tab[r * 16 + wave] + __popcll(m & ((1ull << lane) - 1))] = item[r];
+      for (int r = 0; r < kSlice; ++r) {
+        const bool sel = kr[r] == k;
+        const unsigned long long m = __ballot(sel);
+        if (sel) list[tab[(k * kSlice + r) * 16 + wave] + __popcll(m & ((1ull << lane) - 1))] = item[r];
+      }
     }
-    run += slice_total;
-    __syncthreads();  // tab and slice_total are rewritten by the next slice
+    __syncthreads();  // tab is rewritten by the next slice
   }
 }
 

@@ -189,3 +189,37 @@ def test_uniform_packs_of_4_at_d64_full_oracle(case):
     say(f"  {name}: max_abs={err.max():.3e} mean_abs={err.mean():.3e}")
     assert np.all(np.isfinite(got))
     assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+# name, B, heads (Hq = Hkv), S: more than 16,384 single-head items (the XCD
+# bucket pass takes the work order in two slices), with 5 heads per bucket
+# (one head range each) and with 18 heads per bucket (8 ranges of up to 3)
+BUCKET_RANGES = [("5_heads_per_bucket_s32768", 1, 40, 32768),
+                 ("18_heads_per_bucket_s8192", 2, 72, 8192)]
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("case", BUCKET_RANGES, ids=[c[0] for c in BUCKET_RANGES])
+def test_single_head_buckets_in_head_ranges(case):
+    """Single-head items dealt to the XCD buckets head range by head range:
+    every output element written (NaN-prefilled output), sampled rows of the
+    first and last heads of several buckets against the oracle."""
+    name, B, H, S = case
+    D = 64
+    nQB = S // 64
+    assert B * H * nQB > 16384
+    rng = np.random.default_rng(B * H + S)
+    m = workloads.random_block_mask(rng, B, H, nQB, nQB, p=0.05)
+    m[:, :, np.arange(nQB), np.arange(nQB)] = 1  # every row has its diagonal block
+    q, k, v = small_qkv(41, B, H, H, S, S, D)
+    scale = 1.0 / math.sqrt(D)
+    say(f"[parity-full] bucket head ranges: {name}, {B * H * nQB} single-head items")
+    got = fused(q, k, v, m, scale, True)
+    assert np.all(np.isfinite(got)), "an output element was never written"
+    rows = np.r_[0, 63, 64, S - 1, rng.integers(0, S, 24)]
+    heads = [(b, h) for b in range(B) for h in (0, 7, 8, H - 1)]
+    idx = np.array([(b, h, r) for b, h in heads for r in rows], dtype=np.int64)
+    want = oracle.attention_rows(q, k, v, idx, m, scale, True, 64)
+    err = np.abs(got[idx[:, 0], idx[:, 1], idx[:, 2]].astype(np.float64) - want)
+    say(f"  {name}: sampled rows: max_abs={err.max():.3e} mean_abs={err.mean():.3e}")
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
