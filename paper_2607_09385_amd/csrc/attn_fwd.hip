@@ -39,13 +39,22 @@ namespace steel {
 template <int PACK>
 constexpr int stages_for() { return PACK == 1 ? 2 : 4; }
 
-// Key halves per row half: a single head at D = 128 in bf16 splits every
-// tile's keys over two wave pairs (see k_attn); everything else keeps whole
-// tiles per wave.
-template <int D, int PACK, int PREC>
-constexpr int key_halves() { return PACK == 1 && D == 128 && PREC == kBf16 ? 2 : 1; }
-template <int D, int PACK, int PREC>
-constexpr int attn_threads() { return 128 * PACK * key_halves<D, PACK, PREC>(); }
+// Key halves per row half: a single head in bf16 splits every tile's keys
+// over two wave pairs (see k_attn) at D = 128, and at D = 64 when S_k is a
+// multiple of the block (the ragged copy's registers would not fit four
+// waves per SIMD); everything else keeps whole tiles per wave.
+template <int D, int PACK, int PREC, bool RAGGED>
+constexpr int key_halves() {
+  return PACK == 1 && PREC == kBf16 && (D == 128 || !RAGGED) ? 2 : 1;
+}
+template <int D, int PACK, int PREC, bool RAGGED>
+constexpr int attn_threads() { return 128 * PACK * key_halves<D, PACK, PREC, RAGGED>(); }
+// Waves per SIMD the register allocation must allow: the key-split D = 64
+// kernel is built for four (128 VGPRs), so that four of its workgroups (16
+// waves, the 2-stage rings filling 128 KiB of LDS) share a CU; 1 leaves the
+// allocation free.
+template <int D, int PACK, int PREC, bool RAGGED>
+constexpr int attn_min_waves() { return D == 64 && key_halves<D, PACK, PREC, RAGGED>() == 2 ? 4 : 1; }
 
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 
@@ -136,15 +145,19 @@ __device__ __forceinline__ void merge_halves(const AttnArgs& a, f32x16 (&o)[D / 
 // the keys of every tile are split as well: waves 0-1 take keys 0-31, waves
 // 2-3 keys 32-63, each with its own softmax state, and the two states of a
 // row are merged at the end (the split-key form of the same recurrence, exact
-// up to rounding).  At D = 64 several two-wave workgroups share a CU already.
+// up to rounding).  A single head at D = 64 splits its keys the same way when
+// S_k is aligned: each wave then holds half the scores and fits in 128 VGPRs,
+// so four waves share each SIMD (twice the softmax issue of the two-wave
+// form, whose four workgroups per CU left two per SIMD).
 // RAGGED: S_k is not a multiple of the block (the
 // tail block's copies clamp their rows); without it that path is compiled out.
 template <int D, int PACK, bool RAGGED, int PREC>
-__global__ __launch_bounds__((attn_threads<D, PACK, PREC>())) void k_attn(AttnArgs a) {
+__global__ __launch_bounds__((attn_threads<D, PACK, PREC, RAGGED>()))
+__attribute__((amdgpu_waves_per_eu(attn_min_waves<D, PACK, PREC, RAGGED>()))) void k_attn(AttnArgs a) {
   constexpr bool QK8 = PREC == kFp8All;  // S = K Q^T from E4M3 operands
   constexpr bool PV8 = PREC != kBf16;    // O += V P from E4M3 operands
   constexpr int NT = 1;            // 32-row N-tiles per wave
-  constexpr int KH = key_halves<D, PACK, PREC>();  // key halves (waves per 32 rows)
+  constexpr int KH = key_halves<D, PACK, PREC, RAGGED>();  // key halves (waves per 32 rows)
   constexpr int NSG = 2 / KH;      // 32-key sub-tiles per wave and tile
   constexpr int NW = PACK * 2 * KH;  // waves
   constexpr int C = D / 8;         // 16-byte chunks per bf16 row
@@ -647,18 +660,22 @@ static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   if (grid <= 0) return;
   // the bucket-dealt single-head list: grid is already 8 x (largest bucket)
   const int g = PACK == 1 && a.bucket != nullptr ? grid : xcd_grid(grid);
-  constexpr int threads = attn_threads<D, PACK, PREC>();
   // E4M3 tiles are padded with zero keys: with both tensors in E4M3 no copy
-  // clamps.  At D = 64 the copy of the bf16 kernel without the ragged path
-  // needs fewer registers (162 vs 178), so a third wave fits on each SIMD,
-  // and it ran 4.6% slower on the 24-head S = 32768 workload: D = 64 keeps
-  // the one variant.
+  // clamps.  The whole-tile D = 64 kernels keep the ragged copy for every
+  // S_k: without it they need fewer registers, a third wave fits on each
+  // SIMD, and the single-head kernel ran 4.6% slower that way on the
+  // 24-head S = 32768 workload.  The key-split single-head D = 64 kernel
+  // (aligned S_k) has its own register budget.
+  constexpr bool kRaggedAlways = D == 64 && !(PACK == 1 && PREC == kBf16);
   if constexpr (PREC == kFp8All)
-    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g), dim3(threads), 0, s, a);
-  else if (D == 64 || a.S_k % kBlk != 0)
-    hipLaunchKernelGGL((k_attn<D, PACK, true, PREC>), dim3(g), dim3(threads), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g),
+                       dim3(attn_threads<D, PACK, PREC, false>()), 0, s, a);
+  else if (kRaggedAlways || a.S_k % kBlk != 0)
+    hipLaunchKernelGGL((k_attn<D, PACK, true, PREC>), dim3(g),
+                       dim3(attn_threads<D, PACK, PREC, true>()), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g), dim3(threads), 0, s, a);
+    hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g),
+                       dim3(attn_threads<D, PACK, PREC, false>()), 0, s, a);
 }
 
 template <int D, int PREC>
