@@ -40,13 +40,10 @@ template <int PACK>
 constexpr int stages_for() { return PACK == 1 ? 2 : 4; }
 
 // Key halves per row half: a single head in bf16 splits every tile's keys
-// over two wave pairs (see k_attn) at D = 128, and at D = 64 when S_k is a
-// multiple of the block (the ragged copy's registers would not fit four
-// waves per SIMD); everything else keeps whole tiles per wave.
+// over two wave pairs (see k_attn); everything else keeps whole tiles per
+// wave.
 template <int D, int PACK, int PREC, bool RAGGED>
-constexpr int key_halves() {
-  return PACK == 1 && PREC == kBf16 && (D == 128 || !RAGGED) ? 2 : 1;
-}
+constexpr int key_halves() { return PACK == 1 && PREC == kBf16 ? 2 : 1; }
 template <int D, int PACK, int PREC, bool RAGGED>
 constexpr int attn_threads() { return 128 * PACK * key_halves<D, PACK, PREC, RAGGED>(); }
 // Waves per SIMD the register allocation must allow: the key-split D = 64
@@ -145,10 +142,10 @@ __device__ __forceinline__ void merge_halves(const AttnArgs& a, f32x16 (&o)[D / 
 // the keys of every tile are split as well: waves 0-1 take keys 0-31, waves
 // 2-3 keys 32-63, each with its own softmax state, and the two states of a
 // row are merged at the end (the split-key form of the same recurrence, exact
-// up to rounding).  A single head at D = 64 splits its keys the same way when
-// S_k is aligned: each wave then holds half the scores and fits in 128 VGPRs,
-// so four waves share each SIMD (twice the softmax issue of the two-wave
-// form, whose four workgroups per CU left two per SIMD).
+// up to rounding).  A single head at D = 64 splits its keys the same way:
+// each wave then holds half the scores and fits in 128 VGPRs, so four waves
+// share each SIMD (twice the softmax issue of the two-wave form, whose four
+// workgroups per CU left two per SIMD).
 // RAGGED: S_k is not a multiple of the block (the
 // tail block's copies clamp their rows); without it that path is compiled out.
 template <int D, int PACK, bool RAGGED, int PREC>
@@ -613,10 +610,15 @@ __attribute__((amdgpu_waves_per_eu(attn_min_waves<D, PACK, PREC, RAGGED>()))) vo
       if (u == 3 && ST > 3) step(i + 3, Par<(3 % ST)>{});
     }
   }
-  for (int u = 0; i < L; ++i, ++u) {
-    if (u == 0) step(i, Par<0>{});
-    else if (u == 1) step(i, Par<(1 % ST)>{});
-    else if (u == 2) step(i, Par<(2 % ST)>{});
+  // the last L % ST tiles (i is a multiple of ST here)
+  if constexpr (ST == 2) {
+    if (i < L) step(i, Par<0>{});
+  } else {
+    for (int u = 0; i < L; ++i, ++u) {
+      if (u == 0) step(i, Par<0>{});
+      else if (u == 1) step(i, Par<(1 % ST)>{});
+      else if (u == 2) step(i, Par<(2 % ST)>{});
+    }
   }
 
   if constexpr (KH == 2) {
@@ -663,9 +665,9 @@ static void launch_one(const AttnArgs& a, int grid, hipStream_t s) {
   // E4M3 tiles are padded with zero keys: with both tensors in E4M3 no copy
   // clamps.  The whole-tile D = 64 kernels keep the ragged copy for every
   // S_k: without it they need fewer registers, a third wave fits on each
-  // SIMD, and the single-head kernel ran 4.6% slower that way on the
-  // 24-head S = 32768 workload.  The key-split single-head D = 64 kernel
-  // (aligned S_k) has its own register budget.
+  // SIMD, and the two-wave single-head kernel ran 4.6% slower that way on
+  // the 24-head S = 32768 workload.  The key-split single-head D = 64 kernel
+  // has its own register budget.
   constexpr bool kRaggedAlways = D == 64 && !(PACK == 1 && PREC == kBf16);
   if constexpr (PREC == kFp8All)
     hipLaunchKernelGGL((k_attn<D, PACK, false, PREC>), dim3(g),
