@@ -439,6 +439,16 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
     q += (rem >= rows_per_g) - (rem < 0);
     return q;
   };
+  // head range of group g of this bucket: (g / 8) / per = g / (8 per), the
+  // same corrected double quotient
+  const int range_div = kBuckets * per;
+  const double inv_range = 1.0 / (double)range_div;
+  auto range_of = [&](int g) {
+    int q = (int)((double)g * inv_range);
+    const int rem = g - q * range_div;
+    q += (rem >= range_div) - (rem < 0);
+    return q;
+  };
   if (t < kKeys) key_n[t] = 0;
   __syncthreads();
   // item[r]: the order entry of round r; kr[r]: its head range when it is in
@@ -456,8 +466,7 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
       const int g = item[r] < 0 ? -1 : group_of(item[r]);
       const int bk = g & (kBuckets - 1);
       below += g >= 0 && bk < mb;
-      const int sub = g / kBuckets;
-      kr[r] = g >= 0 && bk == mb ? (per == 1 ? sub : sub / per) : -1;
+      kr[r] = g >= 0 && bk == mb ? range_of(g) : -1;
     }
     return below;
   };
