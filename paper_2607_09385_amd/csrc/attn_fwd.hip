@@ -685,7 +685,7 @@ static hipError_t launch_d(const Problem& p, AttnArgs a, const IndexBuffers& w, 
   if (p.pack > 1) {
     AttnArgs ap = a;
     ap.order = w.order_p;
-    ap.n_items = w.n_items + 1;
+    ap.n_items = w.n_items + kPackItems;  // 0 when k_bucket handed them to the single-head list
     if (p.pack == 2) {
       launch_one<D, 2, PREC>(ap, p.NP, s);
     } else if (D == 128 && (size_t)p.S_q * D * 4 < (1ull << 31)) {

@@ -175,6 +175,7 @@ __device__ __forceinline__ void write_header(const Problem& p, int32_t* n_items)
   h[kPfHkv] = p.Hkv;
   h[kPfSq] = p.S_q;
   h[kPfSk] = p.S_k;
+  n_items[kPackItems] = n_items[1];  // k_bucket may take them over
 }
 
 // Histogram index of (bin, chunk): bins descending from the list's top bin,
@@ -413,7 +414,8 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
 // count, one wave per range scans its (round, wave) counts into bases, and
 // every item goes to its base plus the count of its wave's earlier lanes.
 __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
-                                                 const int32_t* __restrict__ n_items,
+                                                 const int32_t* __restrict__ order_p,
+                                                 int32_t* __restrict__ n_items,
                                                  int32_t* __restrict__ bucket) {
   constexpr int kSlice = 16;                // rounds of 1024 items per slice
   constexpr int kKeys = 8;                  // head ranges per bucket, at most
@@ -421,6 +423,7 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
   __shared__ int red[16];
   __shared__ int key_n[kKeys];     // this bucket's items per range
   __shared__ int key_base[kKeys];  // list position of the range's next item
+  __shared__ int demoted_at;       // list position of this bucket's first pack row
   const int mb = (int)blockIdx.x;  // this workgroup's bucket
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = n_items[0];
@@ -450,6 +453,25 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
     return q;
   };
   if (t < kKeys) key_n[t] = 0;
+  // A short head-pack list (fewer than kDemotePacks items) joins a long
+  // single-head list (at least kDemoteMinSingle items, so the single-head
+  // kernel runs): wave 0 takes one pack item per lane; its pack rows go after
+  // the bucket's single-head items.
+  const int np = n_items[1];
+  const bool demote = p.pack > 1 && !p.heads_share_mask && np > 0 && np < kDemotePacks &&
+                      n_items[0] >= kDemoteMinSingle;
+  int d_item = -1, d_below = 0, d_own = 0, d_rank = 0;
+  if (demote && wave == 0) {
+    d_item = lane < np ? order_p[lane] : -1;
+    const int bh0 = d_item < 0 ? 0 : (d_item / p.nQB) * p.pack;  // b*Hq + first head
+    const int bk = (bh0 / p.G) & (kBuckets - 1);                 // bucket of b*Hkv + g
+    const unsigned long long mine = __ballot(d_item >= 0 && bk == mb);
+    d_below = __popcll(__ballot(d_item >= 0 && bk < mb));
+    d_own = __popcll(mine);
+    d_rank = __popcll(mine & ((1ull << lane) - 1));
+    if (!(d_item >= 0 && bk == mb)) d_item = -1;
+  }
+  if (mb == 0 && t == 0 && demote) n_items[kPackItems] = 0;  // the pack kernels take none
   __syncthreads();
   // item[r]: the order entry of round r; kr[r]: its head range when it is in
   // this bucket, else -1.  Returns the thread's count of lower-bucket items.
@@ -487,18 +509,24 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
   if (lane == 0) red[wave] = below;
   __syncthreads();
   if (t == 0) {
-    int run = 0;
+    int run = p.pack * d_below;  // pack rows of lower buckets
     for (int w = 0; w < 16; ++w) run += red[w];
     bucket[mb] = run;
     for (int k = 0; k < nkey; ++k) {
       key_base[k] = run;
       run += key_n[k];
     }
+    demoted_at = run;
+    run += p.pack * d_own;
     if (mb == kBuckets - 1) bucket[kBuckets] = run;
   }
   __syncthreads();
-  // pass 2: this bucket's items in range order, one slice at a time
   int32_t* list = bucket + kBuckets + 1;
+  if (d_item >= 0) {  // this bucket's pack items: their rows, one item per lane
+    const int qb = d_item % p.nQB, bh0 = (d_item / p.nQB) * p.pack;
+    for (int h = 0; h < p.pack; ++h) list[demoted_at + d_rank * p.pack + h] = (bh0 + h) * p.nQB + qb;
+  }
+  // pass 2: this bucket's items in range order, one slice at a time
   for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
     if (!one) load(s0);
 #pragma unroll 1
@@ -565,7 +593,8 @@ hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const Index
                      wide, w.cnt, w.row_ptr, w.col, w.hist_s, w.hist_p, w.n_items, w.order_s,
                      w.order_p, rows_grid, nch_s);
   if (w.bucket != nullptr)
-    hipLaunchKernelGGL(k_bucket, dim3(kBuckets), dim3(1024), 0, s, p, w.order_s, w.n_items, w.bucket);
+    hipLaunchKernelGGL(k_bucket, dim3(kBuckets), dim3(1024), 0, s, p, w.order_s, w.order_p, w.n_items,
+                       w.bucket);
   return hipGetLastError();
 }
 

@@ -102,7 +102,8 @@ struct IndexBuffers {
   int32_t* order_s;    // [R]   single-head items, heaviest first
   int32_t* order_p;    // [NP]  head-pack items, heaviest first
   int32_t* n_items;    // [kHeaderInts] {single items, pack items, plan header,
-                       //   top bins of the two lists} (see kPlanAt, kTopBin)
+                       //   top bins of the two lists, pack items the pack
+                       //   kernels take} (see kPlanAt, kTopBin, kPackItems)
   // single-head items dealt to the 8 XCDs by key/value head (nullptr: none):
   // [kBuckets + 1] bucket starts, then the items of order_s stably
   // partitioned by bucket
@@ -119,13 +120,25 @@ constexpr int kBuckets = 8;
 // other sizes, another causal limit or another head packing than the plan
 // leaves its output untouched.  Layout of n_items: [0] single-head items,
 // [1] head-pack items, [kPlanAt + f] field f of PlanField, [kTopBin + list]
-// the top work-order bin of each list.
+// the top work-order bin of each list, [kPackItems] the head-pack items the
+// pack kernels take (n_items[1], or 0 when k_bucket hands a short pack list
+// to the single-head kernel, see kDemotePacks).
 constexpr int kPlanMagic = 0x5354454c;  // "STEL"
 enum PlanField { kPfMagic, kPfR, kPfNKB, kPfPack, kPfCausal, kPfDelta, kPfB, kPfHq, kPfHkv,
                  kPfSq, kPfSk, kPlanFields };
 constexpr int kPlanAt = 2;
 constexpr int kTopBin = kPlanAt + kPlanFields;
-constexpr int kHeaderInts = kTopBin + 2;
+constexpr int kPackItems = kTopBin + 2;
+constexpr int kHeaderInts = kPackItems + 1;
+
+// A head-pack list shorter than kDemotePacks (a quarter of the CUs) is run
+// by the single-head kernel, as pack-many rows per item, when that kernel
+// has at least kDemoteMinSingle items of its own: a pack kernel for a few
+// items would add one item's latency to the run while most CUs idle, and the
+// single-head kernel absorbs the rows.  The rows of a uniform pack have one
+// live list, so either kernel computes the same rows.
+constexpr int kDemotePacks = 64;
+constexpr int kDemoteMinSingle = 1024;
 
 __host__ __device__ inline int nchunks(int n) { return (n + kChunk - 1) / kChunk; }
 

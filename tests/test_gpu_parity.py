@@ -80,6 +80,8 @@ SMALL = [
     ("tiny_S1", 1, 1, 1, 1, 1, 64, True, "none"),
     ("S65_D128", 3, 3, 1, 65, 65, 128, True, "none"),
     ("noncausal_masked", 1, 2, 2, 448, 448, 128, False, "random"),
+    # mixed head packs, 126 of them uniform
+    ("gqa4_mixed_packs_126", 2, 16, 4, 1024, 1024, 128, True, "mixed"),
     # single heads at D = 64 with S_k a multiple of 64 (the key-split kernel)
     ("sq_gt_sk_aligned_d64", 1, 2, 2, 256, 128, 64, True, "random"),
     ("sq_lt_sk_aligned_d64_noncausal", 2, 3, 3, 128, 320, 64, False, "random"),

@@ -223,3 +223,39 @@ def test_single_head_buckets_in_head_ranges(case):
     err = np.abs(got[idx[:, 0], idx[:, 1], idx[:, 2]].astype(np.float64) - want)
     say(f"  {name}: sampled rows: max_abs={err.max():.3e} mean_abs={err.mean():.3e}")
     assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
+
+
+@pytest.mark.timeout(600)
+def test_short_pack_list_among_many_single_head_rows():
+    """A few uniform head packs (fewer than 64) among at least 1,024
+    single-head items: the packs' rows are dealt with the single-head items.
+    NaN-prefilled output all finite; every row of every uniform pack and
+    sampled other rows against the oracle."""
+    B, Hq, Hkv, S, D = 2, 16, 4, 4096, 128
+    G = Hq // Hkv
+    nQB = S // 64
+    rng = np.random.default_rng(77)
+    m = workloads.random_block_mask(rng, B, Hq, nQB, nQB, p=0.3)
+    i = np.arange(nQB)
+    m[:, :, i, i] = 1
+    for _ in range(12):  # a dozen more uniform packs: one head's row copied to its group
+        b, g, qb = int(rng.integers(B)), int(rng.integers(Hkv)), int(rng.integers(nQB))
+        m[b, G * g + 1:G * g + G, qb, :] = m[b, G * g, qb, :]
+    alive = np.tril(np.ones((nQB, nQB), dtype=bool))
+    live = (m != 0) & alive
+    uniform = [(b, g, qb) for b in range(B) for g in range(Hkv) for qb in range(nQB)
+               if all(np.array_equal(live[b, G * g, qb], live[b, G * g + h, qb]) for h in range(1, G))]
+    n_single = B * Hq * nQB - G * len(uniform)
+    assert 0 < len(uniform) < 64 and n_single >= 1024, (len(uniform), n_single)
+    q, k, v = small_qkv(43, B, Hq, Hkv, S, S, D)
+    scale = 1.0 / math.sqrt(D)
+    say(f"[parity-full] short pack list: {len(uniform)} uniform packs, {n_single} single-head rows")
+    got = fused(q, k, v, m, scale, True)
+    assert np.all(np.isfinite(got)), "an output element was never written"
+    idx = [(b, G * g + h, 64 * qb + r) for b, g, qb in uniform for h in range(G) for r in range(64)]
+    idx += [(int(rng.integers(B)), int(rng.integers(Hq)), int(rng.integers(S))) for _ in range(256)]
+    idx = np.array(idx, dtype=np.int64)
+    want = oracle.attention_rows(q, k, v, idx, m, scale, True, 64)
+    err = np.abs(got[idx[:, 0], idx[:, 1], idx[:, 2]].astype(np.float64) - want)
+    say(f"  {len(idx)} rows: max_abs={err.max():.3e} mean_abs={err.mean():.3e}")
+    assert err.max() <= MAX_ABS and err.mean() <= MEAN_ABS
