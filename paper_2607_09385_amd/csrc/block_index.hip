@@ -397,41 +397,38 @@ __global__ __launch_bounds__(256) void k_fill_scatter(
   order[base[hist_at(bin, c, nch, top)] + rank] = item;
 }
 
-// Stable partition of the single-head work order into the XCD buckets, one
-// 1024-thread workgroup per bucket.  The bucket of row r is g % 8, with
-// g = r / (nQB*G) = b*Hkv + (key/value head).  Within a bucket the items go
-// head by head: the bucket's heads g = mb, mb + 8, ... fall into at most kKeys
-// consecutive ranges (one head per range when a bucket holds at most kKeys
-// heads), the ranges in increasing g, and within a range the items keep the
-// heaviest-first order.  The workgroups an XCD runs at one time then read the
-// key/value tiles of one head, which its L2 keeps, instead of those of all
-// the bucket's heads.
-// Each workgroup takes the order in slices of kSlice rounds of 1024 items
-// (one per thread and round, the loads of a slice issued together; a
-// 12,288-item order is one slice, loaded once).  A first pass counts the
-// items of lower buckets (this bucket's start) and this bucket's items per
-// range.  Then, per slice and range: one ballot per round gives each wave's
-// count, one wave per range scans its (round, wave) counts into bases, and
-// every item goes to its base plus the count of its wave's earlier lanes.
+// Stable partition of the single-head work order into the XCD buckets.  The
+// bucket of row r is g % 8, with g = r / (nQB*G) = b*Hkv + (key/value head).
+// Within a bucket the items go head by head: the bucket's heads g = mb,
+// mb + 8, ... fall into bucket_ranges(p) consecutive ranges (one head per
+// range when a bucket holds at most kBucketRanges heads), the ranges in
+// increasing g, and within a range the items keep the heaviest-first order.
+// The workgroups an XCD runs at one time then read the key/value tiles of
+// one head, which its L2 keeps, instead of those of all the bucket's heads.
+// One 1024-thread workgroup per (bucket, range).  Each takes the order in
+// slices of kSlice rounds of 1024 items (one per thread and round, the loads
+// of a slice issued together; a 12,288-item order is one slice, loaded
+// once).  A first pass counts the items before its range (lower buckets, and
+// lower ranges of its bucket) and its own.  Then, per slice: one ballot per
+// round gives each wave's count of own items, one wave scans the (round,
+// wave) counts into bases, and every own item goes to its base plus the
+// count of its wave's earlier lanes.
 __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __restrict__ order,
                                                  const int32_t* __restrict__ order_p,
                                                  int32_t* __restrict__ n_items,
                                                  int32_t* __restrict__ bucket) {
-  constexpr int kSlice = 16;                // rounds of 1024 items per slice
-  constexpr int kKeys = 8;                  // head ranges per bucket, at most
-  __shared__ int tab[kKeys * kSlice * 16];  // (range, round, wave) counts, then bases
-  __shared__ int red[16];
-  __shared__ int key_n[kKeys];     // this bucket's items per range
-  __shared__ int key_base[kKeys];  // list position of the range's next item
-  __shared__ int demoted_at;       // list position of this bucket's first pack row
-  const int mb = (int)blockIdx.x;  // this workgroup's bucket
+  constexpr int kSlice = 16;        // rounds of 1024 items per slice
+  __shared__ int tab[kSlice * 16];  // (round, wave) counts, then bases
+  __shared__ int red[3][16];
+  __shared__ int slice_total;
+  const int nkey = bucket_ranges(p);
+  const int mb = (int)blockIdx.x / nkey;  // this workgroup's bucket
+  const int kk = (int)blockIdx.x % nkey;  // and head range
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const int n = n_items[0];
   const int rows_per_g = p.nQB * p.G;
-  const int heads = p.B * p.Hkv;
-  const int nsub = (heads + kBuckets - 1) / kBuckets;  // heads of a bucket, at most
-  const int nkey = nsub < kKeys ? nsub : kKeys;
-  const int per = (nsub + nkey - 1) / nkey;  // heads per range
+  const int nsub = (p.B * p.Hkv + kBuckets - 1) / kBuckets;  // heads of a bucket, at most
+  const int per = (nsub + nkey - 1) / nkey;                  // heads per range
   // r / rows_per_g without an integer division (a long instruction sequence
   // per item): the double quotient is within one of the truth for r < 2^31,
   // and one correction step makes it exact
@@ -442,8 +439,8 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
     q += (rem >= rows_per_g) - (rem < 0);
     return q;
   };
-  // head range of group g of this bucket: (g / 8) / per = g / (8 per), the
-  // same corrected double quotient
+  // head range of group g within its bucket: (g / 8) / per = g / (8 per),
+  // the same corrected double quotient
   const int range_div = kBuckets * per;
   const double inv_range = 1.0 / (double)range_div;
   auto range_of = [&](int g) {
@@ -452,14 +449,14 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
     q += (rem >= range_div) - (rem < 0);
     return q;
   };
-  if (t < kKeys) key_n[t] = 0;
   // A short head-pack list (fewer than kDemotePacks items) joins a long
   // single-head list (at least kDemoteMinSingle items, so the single-head
-  // kernel runs): wave 0 takes one pack item per lane; its pack rows go after
-  // the bucket's single-head items.
+  // kernel runs): wave 0 takes one pack item per lane; the pack rows of a
+  // bucket go after its single-head items, placed by its last range's
+  // workgroup.
   const int np = n_items[1];
   const bool demote = p.pack > 1 && !p.heads_share_mask && np > 0 && np < kDemotePacks &&
-                      n_items[0] >= kDemoteMinSingle;
+                      n >= kDemoteMinSingle;
   int d_item = -1, d_below = 0, d_own = 0, d_rank = 0;
   if (demote && wave == 0) {
     d_item = lane < np ? order_p[lane] : -1;
@@ -471,104 +468,101 @@ __global__ __launch_bounds__(1024) void k_bucket(Problem p, const int32_t* __res
     d_rank = __popcll(mine & ((1ull << lane) - 1));
     if (!(d_item >= 0 && bk == mb)) d_item = -1;
   }
-  if (mb == 0 && t == 0 && demote) n_items[kPackItems] = 0;  // the pack kernels take none
-  __syncthreads();
-  // item[r]: the order entry of round r; kr[r]: its head range when it is in
-  // this bucket, else -1.  Returns the thread's count of lower-bucket items.
-  int item[kSlice], kr[kSlice];
-  auto load = [&](int s0) {
+  if (blockIdx.x == 0 && t == 0 && demote) n_items[kPackItems] = 0;  // the pack kernels take none
+  // item[r]: the order entry of round r; own[r]: it is in this range
+  int item[kSlice], own[kSlice];
+  int below_b = 0, below_r = 0;  // items of lower buckets, of lower ranges of this one
+  auto load = [&](int s0, bool count) {
 #pragma unroll
     for (int r = 0; r < kSlice; ++r) {
       const int i = s0 + 1024 * r + t;
       item[r] = i < n ? order[i] : -1;
     }
-    int below = 0;
 #pragma unroll
     for (int r = 0; r < kSlice; ++r) {
       const int g = item[r] < 0 ? -1 : group_of(item[r]);
       const int bk = g & (kBuckets - 1);
-      below += g >= 0 && bk < mb;
-      kr[r] = g >= 0 && bk == mb ? range_of(g) : -1;
+      const bool in_b = g >= 0 && bk == mb;
+      const int key = in_b ? range_of(g) : -1;
+      if (count) {
+        below_b += g >= 0 && bk < mb;
+        below_r += in_b && key < kk;
+      }
+      own[r] = in_b && key == kk;
     }
-    return below;
   };
   const bool one = n <= kSlice * 1024;  // the whole order stays in registers
-  // pass 1: items of lower buckets, and of this one per range
-  int below = 0;
+  // pass 1: items before this range, and its own
+  int mine = 0;
   for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
-    below += load(s0);
-#pragma unroll 1
-    for (int k = 0; k < nkey; ++k) {
-      int c = 0;
+    load(s0, true);
 #pragma unroll
-      for (int r = 0; r < kSlice; ++r) c += __popcll(__ballot(kr[r] == k));
-      if (lane == 0 && c) atomicAdd(&key_n[k], c);
-    }
+    for (int r = 0; r < kSlice; ++r) mine += own[r];
   }
-  for (int off = 32; off > 0; off >>= 1) below += __shfl_xor(below, off);
-  if (lane == 0) red[wave] = below;
-  __syncthreads();
-  if (t == 0) {
-    int run = p.pack * d_below;  // pack rows of lower buckets
-    for (int w = 0; w < 16; ++w) run += red[w];
-    bucket[mb] = run;
-    for (int k = 0; k < nkey; ++k) {
-      key_base[k] = run;
-      run += key_n[k];
-    }
-    demoted_at = run;
-    run += p.pack * d_own;
-    if (mb == kBuckets - 1) bucket[kBuckets] = run;
+  for (int off = 32; off > 0; off >>= 1) {
+    below_b += __shfl_xor(below_b, off);
+    below_r += __shfl_xor(below_r, off);
+    mine += __shfl_xor(mine, off);
+  }
+  if (lane == 0) {
+    red[0][wave] = below_b;
+    red[1][wave] = below_r;
+    red[2][wave] = mine;
   }
   __syncthreads();
+  int lower = p.pack * d_below, before = 0, total = 0;
+  for (int w = 0; w < 16; ++w) {
+    lower += red[0][w];
+    before += red[1][w];
+    total += red[2][w];
+  }
+  const int start = lower + before;  // list position of this range's first item
   int32_t* list = bucket + kBuckets + 1;
-  if (d_item >= 0) {  // this bucket's pack items: their rows, one item per lane
-    const int qb = d_item % p.nQB, bh0 = (d_item / p.nQB) * p.pack;
-    for (int h = 0; h < p.pack; ++h) list[demoted_at + d_rank * p.pack + h] = (bh0 + h) * p.nQB + qb;
+  if (kk == 0 && t == 0) bucket[mb] = lower;
+  if (kk == nkey - 1) {  // the bucket's pack rows follow its last range
+    const int at = start + total;
+    if (d_item >= 0) {
+      const int qb = d_item % p.nQB, bh0 = (d_item / p.nQB) * p.pack;
+      for (int h = 0; h < p.pack; ++h) list[at + d_rank * p.pack + h] = (bh0 + h) * p.nQB + qb;
+    }
+    if (mb == kBuckets - 1 && t == 0) bucket[kBuckets] = at + p.pack * d_own;
   }
-  // pass 2: this bucket's items in range order, one slice at a time
+  // pass 2: this range's items in order, one slice at a time
+  int run = start;
   for (int s0 = 0; s0 < n; s0 += kSlice * 1024) {
-    if (!one) load(s0);
-#pragma unroll 1
-    for (int k = 0; k < nkey; ++k) {
+    if (!one) load(s0, false);
 #pragma unroll
-      for (int r = 0; r < kSlice; ++r) {
-        const unsigned long long m = __ballot(kr[r] == k);
-        if (lane == 0) tab[(k * kSlice + r) * 16 + wave] = __popcll(m);
-      }
+    for (int r = 0; r < kSlice; ++r) {
+      const unsigned long long m = __ballot(own[r] != 0);
+      if (lane == 0) tab[r * 16 + wave] = __popcll(m);
     }
     __syncthreads();
-    if (wave < nkey) {  // wave k: exclusive scan of range k's 256 (round, wave) counts
-      int* tk = tab + wave * kSlice * 16;
+    if (wave == 0) {  // exclusive scan of the 256 counts in (round, wave) order
       int v[4], sum = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         v[j] = sum;
-        sum += tk[4 * lane + j];
+        sum += tab[4 * lane + j];
       }
       int incl = sum;  // inclusive scan of the lane sums
       for (int off = 1; off < 64; off <<= 1) {
         const int y = __shfl_up(incl, off);
         if (lane >= off) incl += y;
       }
-      const int base = key_base[wave];
-      const int excl = base + incl - sum;
+      const int excl = run + incl - sum;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) tk[4 * lane + j] = excl + v[j];
-      const int slice_n = __shfl(incl, 63);
-      if (lane == 0) key_base[wave] = base + slice_n;  // only this wave touches it
+      for (int j = 0; j < 4; ++j) tab[4 * lane + j] = excl + v[j];
+      if (lane == 63) slice_total = incl;
     }
     __syncthreads();
-#pragma unroll 1
-    for (int k = 0; k < nkey; ++k) {
 #pragma unroll
-      for (int r = 0; r < kSlice; ++r) {
-        const bool sel = kr[r] == k;
-        const unsigned long long m = __ballot(sel);
-        if (sel) list[tab[(k * kSlice + r) * 16 + wave] + __popcll(m & ((1ull << lane) - 1))] = item[r];
-      }
+    for (int r = 0; r < kSlice; ++r) {
+      const bool sel = own[r] != 0;
+      const unsigned long long m = __ballot(sel);
+      if (sel) list[tab[r * 16 + wave] + __popcll(m & ((1ull << lane) - 1))] = item[r];
     }
-    __syncthreads();  // tab is rewritten by the next slice
+    run += slice_total;
+    __syncthreads();  // tab and slice_total are rewritten by the next slice
   }
 }
 
@@ -593,8 +587,8 @@ hipError_t launch_block_index(const Problem& p, const uint8_t* mask, const Index
                      wide, w.cnt, w.row_ptr, w.col, w.hist_s, w.hist_p, w.n_items, w.order_s,
                      w.order_p, rows_grid, nch_s);
   if (w.bucket != nullptr)
-    hipLaunchKernelGGL(k_bucket, dim3(kBuckets), dim3(1024), 0, s, p, w.order_s, w.order_p, w.n_items,
-                       w.bucket);
+    hipLaunchKernelGGL(k_bucket, dim3(kBuckets * bucket_ranges(p)), dim3(1024), 0, s, p, w.order_s,
+                       w.order_p, w.n_items, w.bucket);
   return hipGetLastError();
 }
 

@@ -115,6 +115,14 @@ struct IndexBuffers {
 // its L2 keeps them.
 constexpr int kBuckets = 8;
 
+// Head ranges of a bucket: its key/value heads g = mb, mb + 8, ... (at most
+// ceil(B*Hkv / 8)) split into at most kBucketRanges consecutive ranges.
+constexpr int kBucketRanges = 8;
+__host__ __device__ inline int bucket_ranges(const Problem& p) {
+  const int nsub = (p.B * p.Hkv + kBuckets - 1) / kBuckets;
+  return nsub < kBucketRanges ? nsub : kBucketRanges;
+}
+
 // Plan header written after the two item counts; the attention kernels check
 // it against their own arguments before touching the index, so a run with
 // other sizes, another causal limit or another head packing than the plan
