@@ -92,12 +92,13 @@ def traffic_for(workload):
 # Softmax work per element of a live tile: one exp2, the fma that forms its
 # argument, and half each of a 3-input max, a packed bf16 conversion and a bf16
 # dot2 for the row sum.  Cycles per 64-lane instruction measured by
-# `bench.py --mfma-peak` (steel_valu_rate, shader clock): a SIMD with eight
-# resident waves sustains v_exp_f32 every 2.6 cycles and v_fma_f32 every 1.56,
-# while a single wave issues them only every 14.5 and 9.0 cycles (the other
-# three instructions are taken at the fma's rate).
-VALU_CYCLES_SIMD = 2.6 + 1.56 + 1.5 * 1.56        # per 64 elements, SIMD throughput
-VALU_CYCLES_ONE_WAVE = 14.5 + 9.0 + 1.5 * 9.0     # per 64 elements, issued by one wave
+# `bench.py --mfma-peak` (steel_valu_rate, shader clock, from the first wave's
+# start to the last wave's end): a SIMD with eight resident waves sustains
+# v_exp_f32 every 5.26 cycles and v_fma_f32 every 1.98, while a single wave
+# issues them only every 12.0 and 8.5 cycles (the other three instructions are
+# taken at the fma's rate).
+VALU_CYCLES_SIMD = 5.26 + 1.98 + 1.5 * 1.98       # per 64 elements, SIMD throughput
+VALU_CYCLES_ONE_WAVE = 12.0 + 8.5 + 1.5 * 8.5     # per 64 elements, issued by one wave
 
 
 def valu_bound(n_live, D):
@@ -111,10 +112,10 @@ def valu_bound(n_live, D):
     one = (elems * VALU_CYCLES_ONE_WAVE / 64 + n_live * (D // 4) * 32) / (256 * 4 * 2.4e9) * 1e6
     return {"bound": "alu", "us": round(us, 1),
             "model": "per live element: exp2 + fma + half max3 + half cvt_pk_bf16 + half dot2 at the measured "
-                     "SIMD rates (v_exp_f32 2.6, v_fma_f32 1.56 cycles per 64 lanes)",
+                     "SIMD rates (v_exp_f32 5.26, v_fma_f32 1.98 cycles per 64 lanes)",
             "one_wave_softmax_us": round(one, 1),
-            "one_wave_model": "same instructions issued by one wave per SIMD (v_exp_f32 every 14.5, others every "
-                              "9.0 cycles) plus that wave's D/4 score MFMAs per tile (32 cycles each)",
+            "one_wave_model": "same instructions issued by one wave per SIMD (v_exp_f32 every 12.0, others every "
+                              "8.5 cycles) plus that wave's D/4 score MFMAs per tile (32 cycles each)",
             "mfma_us_at_peak": round(4.0 * 64 * 64 * D * n_live / PEAK_TFLOPS / 1e6, 1)}
 
 
@@ -222,7 +223,82 @@ def mfma_peak(iters=400000, waves_per_wg=4):
     res["valu"] = {name: [valu_rate(op, waves_per_wg=w, grid=g)
                           for w, g in ((4, 256), (8, 256), (16, 256), (16, 512))]
                    for op, name in ((0, "v_exp_f32"), (1, "v_fma_f32"))}
+    res["lds"] = {name: [lds_rate(op, waves_per_cu=w) for w in (4, 8, 16)]
+                  for op, name in ((0, "ds_read_b128"), (1, "ds_read_b64_tr_b16"), (2, "ds_write_b128"))}
+    res["copy_to_lds"] = [copy_rate(wg_per_cu=n) for n in (1, 2, 4)]
     return res
+
+
+def _bytes_per_clock(clocks, grid, bytes_per_wg, wall_s):
+    """Bytes per shader-clock cycle per CU, grid / 256 workgroups per CU each
+    moving bytes_per_wg: over the slowest workgroup's loop cycles, and over
+    the launch's wall time (events) at the workgroups' average clock (shader
+    cycles over 100 MHz reference ticks), which also counts the launch."""
+    c = clocks.view(grid, 2).cpu().double()
+    per_cu = (grid / 256) * bytes_per_wg
+    ghz = float((c[:, 0] / (c[:, 1] / 100e6)).mean())
+    return {"loop": round(per_cu / float(c[:, 0].max()), 1),
+            "wall": round(per_cu / (wall_s * ghz), 1)}
+
+
+def _timed(launch):
+    import torch
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    launch()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / 1e3
+
+
+def lds_rate(op, iters=20000, waves_per_cu=16):
+    """LDS rate per CU (steel_lds_rate: op 0 ds_read_b128, 1 two
+    ds_read_b64_tr_b16, 2 ds_write_b128, 16 bytes per lane eight times per
+    iteration) with waves_per_cu waves resident on every CU (256 workgroups)."""
+    import torch
+    from paper_2607_09385_amd import _lib
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    grid = 256
+    sink = torch.empty(grid * 64 * waves_per_cu, dtype=torch.int32, device=dev)
+    clocks = torch.zeros(2 * grid, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    def launch(n=iters):
+        st = lib.steel_lds_rate(op, n, grid, waves_per_cu, sink.data_ptr(), clocks.data_ptr(),
+                                stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"steel_lds_rate failed ({st})")
+    launch(iters // 4)
+    wall = _timed(launch)
+    return {"waves_per_cu": waves_per_cu,
+            "bytes_per_clock_per_cu": _bytes_per_clock(clocks, grid, waves_per_cu * 64 * 16 * 8 * iters,
+                                                       wall)}
+
+
+def copy_rate(iters=1500, wg_per_cu=2, waves_per_wg=4):
+    """Global -> LDS copy rate per CU (steel_copy_rate: global_load_lds_dwordx4
+    filling a 32 KiB buffer per workgroup, waiting for each fill) from a 16 MiB
+    source the L2s hold, with wg_per_cu workgroups of waves_per_wg waves on
+    every CU."""
+    import torch
+    from paper_2607_09385_amd import _lib
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    grid = 256 * wg_per_cu
+    src = torch.ones(16 << 20, dtype=torch.uint8, device=dev)
+    sink = torch.empty(grid * 64 * waves_per_wg, dtype=torch.int32, device=dev)
+    clocks = torch.zeros(2 * grid, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    def launch(n=iters):
+        st = lib.steel_copy_rate(src.data_ptr(), src.numel(), n, grid, waves_per_wg, sink.data_ptr(),
+                                 clocks.data_ptr(), stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"steel_copy_rate failed ({st})")
+    launch(iters // 4)
+    wall = _timed(launch)
+    return {"workgroups_per_cu": wg_per_cu, "waves_per_wg": waves_per_wg,
+            "bytes_per_clock_per_cu": _bytes_per_clock(clocks, grid, 32768 * iters, wall)}
 
 
 def valu_rate(op, iters=200000, waves_per_wg=16, grid=256):

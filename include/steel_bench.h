@@ -2,14 +2,17 @@
  * libsteel measurement helpers (not part of the attention path): the
  * achievable rate of the bf16 matrix-core instruction the attention kernels
  * use (v_mfma_f32_32x32x16_bf16), as the context for their roofline
- * fraction, and the issue rates of the softmax's exponential and fma
- * (v_exp_f32, v_fma_f32), the basis of the plain-ALU estimate.  The paper measures against its device's
- * peak (Section V-A); here the published peak (256 CU x 2.4 GHz x 4096 bf16
+ * fraction, the issue rates of the softmax's exponential and fma
+ * (v_exp_f32, v_fma_f32), the basis of the plain-ALU estimate, and the LDS
+ * and global -> LDS copy rates that the tiles of Algorithm 1 move through.
+ * The paper measures against its device's peak (Section V-A); here the published peak (256 CU x 2.4 GHz x 4096 bf16
  * flop/clk/CU) is the denominator, and the matrix-core rate shows what the
  * chip sustains under the matrix cores' power draw for given operand data.
  */
 #ifndef STEEL_BENCH_H
 #define STEEL_BENCH_H
+
+#include <stddef.h>
 
 #ifdef __cplusplus
 extern "C" {
@@ -53,6 +56,41 @@ int steel_mfma_peak(const void* operands, int iters, int grid, int waves_per_wg,
  */
 int steel_valu_rate(int op, const float* seed, int iters, int grid, int waves_per_wg, float* sink,
                     unsigned long long* clocks, void* stream);
+
+/*
+ * Enqueue grid workgroups of waves_per_wg waves; every lane moves 16 bytes
+ * between its VGPRs and a 32 KiB LDS buffer eight times per iteration, each
+ * time in another 1 KiB block of lane-contiguous slots (no bank conflicts):
+ * op 0 ds_read_b128, op 1 two ds_read_b64_tr_b16 (the transposed reads the
+ * P V product takes its V fragments with), op 2 ds_write_b128.  Bytes moved
+ * per CU over the loop's shader-clock cycles give the LDS rate of that
+ * instruction at that number of resident waves.
+ *
+ *   sink    device uint32 [grid * 64 * waves_per_wg]: one value per lane
+ *   clocks  device uint64 [2 * grid], as for steel_mfma_peak
+ *   stream  hipStream_t as void*, or NULL
+ *
+ * Returns 0 when enqueued, 1 on an invalid argument (nothing enqueued), 3 on
+ * a launch error.
+ */
+int steel_lds_rate(int op, int iters, int grid, int waves_per_wg, unsigned* sink,
+                   unsigned long long* clocks, void* stream);
+
+/*
+ * Enqueue grid workgroups of waves_per_wg waves (1, 2, 4, 8 or 16); each
+ * fills a 32 KiB LDS buffer from src with global_load_lds_dwordx4 (the tile
+ * copy of the attention kernels), waits for its copies, and refills, iters
+ * times.  Workgroup b reads within the (b % 8)-th eighth of src, at offsets
+ * that move by 32 KiB per fill, so a source of a few MiB stays in the L2s.
+ *
+ *   src        device, 16-byte aligned, src_bytes >= 512 KiB
+ *   sink, clocks, stream  as for steel_lds_rate
+ *
+ * Returns 0 when enqueued, 1 on an invalid argument (nothing enqueued), 3 on
+ * a launch error.
+ */
+int steel_copy_rate(const void* src, size_t src_bytes, int iters, int grid, int waves_per_wg,
+                    unsigned* sink, unsigned long long* clocks, void* stream);
 
 #ifdef __cplusplus
 }

@@ -72,6 +72,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_mfma_peak.argtypes = [c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
     lib.steel_valu_rate.restype = c_int
     lib.steel_valu_rate.argtypes = [c_int, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
+    lib.steel_lds_rate.restype = c_int
+    lib.steel_lds_rate.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
+    lib.steel_copy_rate.restype = c_int
+    lib.steel_copy_rate.argtypes = [c_void_p, c_size_t, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
     lib.steel_last_error.restype = ctypes.c_char_p
     lib.steel_last_error.argtypes = []
     lib.steel_version.restype = ctypes.c_char_p

@@ -10,11 +10,14 @@
 //
 // Each workgroup's first lane also records the elapsed shader-clock cycles
 // (s_memtime) and the elapsed 100 MHz reference ticks (s_memrealtime) of its
-// loop, from which the average clock during the run follows.
+// loop, from which the average clock during the run follows.  The same file
+// measures the LDS and global -> LDS copy rates the attention kernels lean
+// on (steel_lds_rate, steel_copy_rate).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 #include "../../include/steel_bench.h"
+#include "attn_common.h"
 
 namespace {
 
@@ -30,6 +33,7 @@ __global__ __launch_bounds__(1024) void k_mfma_peak(const bf16x8* __restrict__ o
   bf16x8 b0 = ops[4 * 64 + lane], b1 = ops[5 * 64 + lane], b2 = ops[6 * 64 + lane],
          b3 = ops[7 * 64 + lane];
   f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  __syncthreads();  // the loop is timed from the first wave's start to the last wave's end
   const unsigned long long t0 = __builtin_amdgcn_s_memtime();
   const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
   for (int it = 0; it < iters; ++it) {
@@ -50,6 +54,7 @@ __global__ __launch_bounds__(1024) void k_mfma_peak(const bf16x8* __restrict__ o
     c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, c2, 0, 0, 0);
     c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a2, b1, c3, 0, 0, 0);
   }
+  __syncthreads();
   const unsigned long long t1 = __builtin_amdgcn_s_memtime();
   const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
   float s = 0.f;
@@ -77,6 +82,7 @@ __global__ __launch_bounds__(1024) void k_valu_rate(const float* __restrict__ se
   float x[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = seed[i] + 0.001f * lane;
+  __syncthreads();  // the loop is timed from the first wave's start to the last wave's end
   const unsigned long long t0 = __builtin_amdgcn_s_memtime();
   const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
   for (int it = 0; it < iters; ++it) {
@@ -86,6 +92,7 @@ __global__ __launch_bounds__(1024) void k_valu_rate(const float* __restrict__ se
       else x[i] = __builtin_fmaf(x[i], 0.999f, 1e-4f);
     }
   }
+  __syncthreads();
   const unsigned long long t1 = __builtin_amdgcn_s_memtime();
   const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
   float s = 0.f;
@@ -98,7 +105,121 @@ __global__ __launch_bounds__(1024) void k_valu_rate(const float* __restrict__ se
   }
 }
 
+// LDS throughput: every wave of a workgroup moves 16 bytes per lane eight
+// times per iteration between VGPRs and a 32 KiB LDS buffer, each time in a
+// different 1 KiB block (lane-contiguous slots, no bank conflicts): op 0
+// ds_read_b128, op 1 two ds_read_b64_tr_b16 (the transposed reads of the V
+// fragments), op 2 ds_write_b128.  Bytes per CU over the shader-clock cycles
+// of the loop give the rate whatever the clock.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
+
+template <int OP>
+__global__ __launch_bounds__(1024) void k_lds_rate(int iters, unsigned* __restrict__ sink,
+                                                   unsigned long long* __restrict__ clocks) {
+  __shared__ __attribute__((aligned(1024))) char buf[32768];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  for (int i = t; i < 32768 / 16; i += blockDim.x) ((u32x4*)buf)[i] = u32x4{(unsigned)i, 1u, 2u, 3u};
+  __syncthreads();
+  u32x4 acc = {0u, 0u, 0u, 0u};
+  s16x4 acc2 = {0, 0, 0, 0};
+  __syncthreads();  // the loop is timed from the first wave's start to the last wave's end
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t off = (uint32_t)((((wave * 8 + j + it) & 31) * 64 + lane) * 16);
+      // volatile: every access is made, none is merged, hoisted or dropped
+      if constexpr (OP == 0) {
+        acc += *(const volatile lds_u32x4*)(buf + off);
+      } else if constexpr (OP == 1) {
+        const s16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(buf + off));
+        const s16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(buf + off + 8));
+        acc2 += a + b;
+      } else {
+        *(volatile lds_u32x4*)(buf + off) = u32x4{(unsigned)it, (unsigned)j, 0u, 0u};
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): the last LDS operations are done
+  __syncthreads();
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  sink[(size_t)blockIdx.x * blockDim.x + t] = acc[0] + acc[1] + (unsigned)(acc2[0] + acc2[1]);
+  if (t == 0) {
+    clocks[2 * (size_t)blockIdx.x] = t1 - t0;
+    clocks[2 * (size_t)blockIdx.x + 1] = r1 - r0;
+  }
+}
+
+// Global -> LDS copy throughput with the attention kernels' copy instruction
+// (global_load_lds_dwordx4): each workgroup fills a 32 KiB LDS buffer from
+// its XCD's eighth of the source (L2-resident when the source is a few MiB),
+// waits for the copies, and starts the next fill at another offset.
+__global__ __launch_bounds__(1024) void k_copy_rate(const char* __restrict__ src, long long region,
+                                                    int iters, unsigned* __restrict__ sink,
+                                                    unsigned long long* __restrict__ clocks) {
+  __shared__ __attribute__((aligned(1024))) char buf[32768];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6, nw = (int)blockDim.x >> 6;
+  const int per = 32 / nw;  // 1 KiB copies per wave per fill
+  const char* base = src + (size_t)(blockIdx.x & 7) * region;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)buf;
+  unsigned acc = 0;
+  __syncthreads();  // the loop is timed from the first wave's start to the last wave's end
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 0; it < iters; ++it) {
+    const long long off = (((long long)(blockIdx.x >> 3) * 7919 * 64 + (long long)it * 32768) %
+                           (region - 32768 + 1)) & ~1023ll;
+    for (int j = 0; j < per; ++j)
+      steel::copy16_to_lds(base + off, (uint32_t)(((wave * per + j) * 64 + lane) * 16),
+                           lds0 + (uint32_t)(wave * per + j) * 1024u);
+    steel::wait_vm<0>();
+    __syncthreads();
+    acc += *(const unsigned*)(buf + ((t * 16 + it * 64) & 32767));
+    __syncthreads();
+  }
+  __syncthreads();
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  sink[(size_t)blockIdx.x * blockDim.x + t] = acc;
+  if (t == 0) {
+    clocks[2 * (size_t)blockIdx.x] = t1 - t0;
+    clocks[2 * (size_t)blockIdx.x + 1] = r1 - r0;
+  }
+}
+
 }  // namespace
+
+extern "C" int steel_lds_rate(int op, int iters, int grid, int waves_per_wg, unsigned* sink,
+                              unsigned long long* clocks, void* stream) {
+  if (op < 0 || op > 2 || !sink || !clocks || iters < 1 || grid < 1 || waves_per_wg < 1 ||
+      waves_per_wg > 16)
+    return 1;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const dim3 g(grid), b(64 * waves_per_wg);
+  if (op == 0) hipLaunchKernelGGL(k_lds_rate<0>, g, b, 0, s, iters, sink, clocks);
+  else if (op == 1) hipLaunchKernelGGL(k_lds_rate<1>, g, b, 0, s, iters, sink, clocks);
+  else hipLaunchKernelGGL(k_lds_rate<2>, g, b, 0, s, iters, sink, clocks);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+extern "C" int steel_copy_rate(const void* src, size_t src_bytes, int iters, int grid,
+                               int waves_per_wg, unsigned* sink, unsigned long long* clocks,
+                               void* stream) {
+  const bool pow2 = waves_per_wg > 0 && (waves_per_wg & (waves_per_wg - 1)) == 0;
+  if (!src || ((uintptr_t)src & 15u) || !sink || !clocks || iters < 1 || grid < 1 || !pow2 ||
+      waves_per_wg > 16 || src_bytes < (size_t)8 * 65536)
+    return 1;
+  const long long region = (long long)(src_bytes / 8) & ~1023ll;  // each XCD's eighth, >= 64 KiB
+  hipLaunchKernelGGL(k_copy_rate, dim3(grid), dim3(64 * waves_per_wg), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const char*>(src), region,
+                     iters, sink, clocks);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
 
 extern "C" int steel_valu_rate(int op, const float* seed, int iters, int grid, int waves_per_wg,
                                float* sink, unsigned long long* clocks, void* stream) {

@@ -41,6 +41,18 @@ def test_mfma_peak_rejects_invalid_before_launch():
     assert lib.steel_mfma_peak(FAKE, 10, 256, 17, FAKE, FAKE, None) == 1
 
 
+def test_lds_and_copy_rate_reject_invalid_before_launch():
+    lib = _lib.load()
+    assert lib.steel_lds_rate(3, 10, 256, 4, FAKE, FAKE, None) == 1
+    assert lib.steel_lds_rate(0, 0, 256, 4, FAKE, FAKE, None) == 1
+    assert lib.steel_lds_rate(0, 10, 256, 17, FAKE, FAKE, None) == 1
+    assert lib.steel_lds_rate(0, 10, 256, 4, None, FAKE, None) == 1
+    assert lib.steel_copy_rate(FAKE, 1 << 20, 10, 256, 3, FAKE, FAKE, None) == 1   # not a power of 2
+    assert lib.steel_copy_rate(FAKE, 1 << 18, 10, 256, 4, FAKE, FAKE, None) == 1   # source too small
+    assert lib.steel_copy_rate(FAKE + 8, 1 << 20, 10, 256, 4, FAKE, FAKE, None) == 1  # misaligned
+    assert lib.steel_copy_rate(None, 1 << 20, 10, 256, 4, FAKE, FAKE, None) == 1
+
+
 def test_version_and_empty_error():
     assert "gfx950" in steel.version()
 
