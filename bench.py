@@ -226,6 +226,7 @@ def mfma_peak(iters=400000, waves_per_wg=4):
     res["lds"] = {name: [lds_rate(op, waves_per_cu=w) for w in (4, 8, 16)]
                   for op, name in ((0, "ds_read_b128"), (1, "ds_read_b64_tr_b16"), (2, "ds_write_b128"))}
     res["copy_to_lds"] = [copy_rate(wg_per_cu=n) for n in (1, 2, 4)]
+    res["mfma_valu_overlap"] = mix_rates()
     return res
 
 
@@ -327,6 +328,48 @@ def valu_rate(op, iters=200000, waves_per_wg=16, grid=256):
     per_instr = float(c[:, 0].mean()) / (iters * 8 * waves_per_simd)
     return {"waves_per_simd": waves_per_simd, "cycles_per_wave_instruction": round(per_instr, 2),
             "finite": bool(torch.isfinite(sink).all().item())}
+
+
+def mix_rates(mfma_iters=2000, valu_iters=1000):
+    """Overlap of one wave's matrix-core work and another wave's VALU work on
+    the same SIMD (steel_mix_rate: one workgroup of eight waves per CU, waves
+    w and w + 4 on SIMD w % 4; waves 0-3 issue v_mfma_f32_32x32x16_bf16 on
+    N(0,1) operands, waves 4-7 eight independent v_exp_f32 or v_fma_f32
+    chains).  Per role: shader-clock cycles per instruction of its own loop,
+    and its average clock; with both roles on, unchanged MFMA cycles mean the
+    VALU work ran beside the matrix core instead of taking turns with it."""
+    import torch
+    from paper_2607_09385_amd import _lib
+    lib = _lib.load()
+    dev = torch.device("cuda:0")
+    grid = 256
+    g = torch.Generator().manual_seed(0)
+    ops = torch.randn((8, 64, 8), generator=g).to(torch.bfloat16).to(dev)
+    seed = torch.linspace(0.2, 0.9, 8, dtype=torch.float32, device=dev)
+    sink = torch.empty(grid * 512, dtype=torch.float32, device=dev)
+    clocks = torch.zeros(2 * 8 * grid, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+    out = {"mfma_per_wave": mfma_iters * 4, "valu_per_wave": valu_iters * 8}
+    for name, mode, vop in (("mfma", 1, 0), ("exp", 2, 0), ("mfma+exp", 3, 0), ("fma", 2, 1),
+                            ("mfma+fma", 3, 1)):
+        for _ in range(2):   # the first launch ramps the clock
+            st = lib.steel_mix_rate(mode, vop, ops.data_ptr(), mfma_iters, seed.data_ptr(), valu_iters,
+                                    grid, sink.data_ptr(), clocks.data_ptr(), stream.cuda_stream)
+            if st != 0:
+                raise RuntimeError(f"steel_mix_rate failed ({st})")
+        torch.cuda.synchronize()
+        c = clocks.view(grid, 8, 2).cpu().double()
+        row = {}
+        if mode & 1:
+            m = c[:, :4]
+            row["mfma_cycles"] = round(float(m[..., 0].mean()) / (mfma_iters * 4), 2)
+            row["mfma_clock_ghz"] = round(float((m[..., 0] / (m[..., 1] / 100e6)).mean() / 1e9), 3)
+        if mode & 2:
+            v = c[:, 4:]
+            row["valu_cycles"] = round(float(v[..., 0].mean()) / (valu_iters * 8), 2)
+            row["valu_clock_ghz"] = round(float((v[..., 0] / (v[..., 1] / 100e6)).mean() / 1e9), 3)
+        out[name] = row
+    return out
 
 
 COPY_BYTES = 256 << 20   # reference elementwise kernel for the counter scale

@@ -92,6 +92,31 @@ int steel_lds_rate(int op, int iters, int grid, int waves_per_wg, unsigned* sink
 int steel_copy_rate(const void* src, size_t src_bytes, int iters, int grid, int waves_per_wg,
                     unsigned* sink, unsigned long long* clocks, void* stream);
 
+/*
+ * Enqueue grid workgroups of eight waves (one per CU for grid = 256); waves
+ * w and w + 4 share SIMD w % 4.  Waves 0-3 run mfma_iters iterations of four
+ * v_mfma_f32_32x32x16_bf16 when bit 0 of mode is set; waves 4-7 run
+ * valu_iters iterations of eight independent VALU chains (vop 0 v_exp_f32,
+ * vop 1 v_fma_f32, as steel_valu_rate) when bit 1 is set (mode 1, 2 or 3).
+ * Comparing each role's cycles with both on against each alone measures how
+ * far one wave's matrix-core work and another wave's VALU work on the same
+ * SIMD overlap.
+ *
+ *   operands  device, as for steel_mfma_peak (fragments 0, 1, 4 and 5 used);
+ *             may be NULL when bit 0 of mode is clear
+ *   seed      device float [8], as for steel_valu_rate; may be NULL when bit
+ *             1 of mode is clear
+ *   sink      device float [grid * 512]: one value per lane
+ *   clocks    device uint64 [2 * 8 * grid]: per wave (workgroup-major),
+ *             shader-clock cycles and 100 MHz reference ticks of its own loop
+ *   stream    hipStream_t as void*, or NULL
+ *
+ * Returns 0 when enqueued, 1 on an invalid argument (nothing enqueued), 3 on
+ * a launch error.
+ */
+int steel_mix_rate(int mode, int vop, const void* operands, int mfma_iters, const float* seed,
+                   int valu_iters, int grid, float* sink, unsigned long long* clocks, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -72,6 +72,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.steel_mfma_peak.argtypes = [c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
     lib.steel_valu_rate.restype = c_int
     lib.steel_valu_rate.argtypes = [c_int, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
+    lib.steel_mix_rate.restype = c_int
+    lib.steel_mix_rate.argtypes = [c_int, c_int, c_void_p, c_int, c_void_p, c_int, c_int, c_void_p,
+                                   c_void_p, c_void_p]
     lib.steel_lds_rate.restype = c_int
     lib.steel_lds_rate.argtypes = [c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]
     lib.steel_copy_rate.restype = c_int

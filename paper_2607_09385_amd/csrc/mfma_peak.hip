@@ -192,6 +192,64 @@ __global__ __launch_bounds__(1024) void k_copy_rate(const char* __restrict__ src
   }
 }
 
+// Overlap of matrix-core and VALU work of two waves on one SIMD: a workgroup
+// of eight waves per CU, waves w and w + 4 on SIMD w % 4.  Waves 0-3 stream
+// v_mfma_f32_32x32x16_bf16 (as k_mfma_peak, four accumulators) when bit 0 of
+// MODE is set; waves 4-7 run the eight-chain loop of k_valu_rate (VOP 0
+// v_exp_f32, 1 v_fma_f32) when bit 1 is set.  Every wave records the
+// shader-clock cycles and reference ticks of its own loop: with both roles
+// on, each role's cycles against its cycles alone show whether the two kinds
+// of work share the SIMD or run side by side (the split the wave-specialised
+// attention kernel is built on).
+template <int MODE, int VOP>
+__global__ __launch_bounds__(512) void k_mix_rate(const bf16x8* __restrict__ ops, int mfma_iters,
+                                                  const float* __restrict__ seed, int valu_iters,
+                                                  float* __restrict__ sink,
+                                                  unsigned long long* __restrict__ clocks) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float s = 0.f;
+  __syncthreads();
+  const unsigned long long t0 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r0 = __builtin_amdgcn_s_memrealtime();
+  if (wave < 4) {
+    if constexpr ((MODE & 1) != 0) {
+      const bf16x8 a0 = ops[0 * 64 + lane], a1 = ops[1 * 64 + lane], b0 = ops[4 * 64 + lane],
+                   b1 = ops[5 * 64 + lane];
+      f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+      for (int it = 0; it < mfma_iters; ++it) {
+        c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b0, c0, 0, 0, 0);
+        c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b1, c1, 0, 0, 0);
+        c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, b1, c2, 0, 0, 0);
+        c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, b0, c3, 0, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+    }
+  } else {
+    if constexpr ((MODE & 2) != 0) {
+      float x[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) x[i] = seed[i] + 0.001f * lane;
+      for (int it = 0; it < valu_iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          if constexpr (VOP == 0) x[i] = __builtin_amdgcn_exp2f(-x[i]);
+          else x[i] = __builtin_fmaf(x[i], 0.999f, 1e-4f);
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s += x[i];
+    }
+  }
+  const unsigned long long t1 = __builtin_amdgcn_s_memtime();
+  const unsigned long long r1 = __builtin_amdgcn_s_memrealtime();
+  sink[(size_t)blockIdx.x * blockDim.x + threadIdx.x] = s;
+  if (lane == 0) {
+    clocks[2 * ((size_t)blockIdx.x * 8 + wave)] = t1 - t0;
+    clocks[2 * ((size_t)blockIdx.x * 8 + wave) + 1] = r1 - r0;
+  }
+}
+
 }  // namespace
 
 extern "C" int steel_lds_rate(int op, int iters, int grid, int waves_per_wg, unsigned* sink,
@@ -243,5 +301,24 @@ extern "C" int steel_mfma_peak(const void* operands, int iters, int grid, int wa
   hipLaunchKernelGGL(k_mfma_peak, dim3(grid), dim3(64 * waves_per_wg), 0,
                      static_cast<hipStream_t>(stream), static_cast<const bf16x8*>(operands), iters,
                      sink, clocks);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+extern "C" int steel_mix_rate(int mode, int vop, const void* operands, int mfma_iters,
+                              const float* seed, int valu_iters, int grid, float* sink,
+                              unsigned long long* clocks, void* stream) {
+  if (mode < 1 || mode > 3 || (vop != 0 && vop != 1) || grid < 1 || !sink || !clocks ||
+      ((mode & 1) && (!operands || mfma_iters < 1)) || ((mode & 2) && (!seed || valu_iters < 1)))
+    return 1;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const bf16x8* ops = static_cast<const bf16x8*>(operands);
+  const dim3 g(grid), b(512);
+#define STEEL_MIX(M, V) hipLaunchKernelGGL((k_mix_rate<M, V>), g, b, 0, s, ops, mfma_iters, seed, valu_iters, sink, clocks)
+  if (mode == 1) STEEL_MIX(1, 0);
+  else if (mode == 2 && vop == 0) STEEL_MIX(2, 0);
+  else if (mode == 2) STEEL_MIX(2, 1);
+  else if (vop == 0) STEEL_MIX(3, 0);
+  else STEEL_MIX(3, 1);
+#undef STEEL_MIX
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }

@@ -43,6 +43,11 @@ def test_mfma_peak_rejects_invalid_before_launch():
 
 def test_lds_and_copy_rate_reject_invalid_before_launch():
     lib = _lib.load()
+    assert lib.steel_mix_rate(0, 0, FAKE, 10, FAKE, 10, 256, FAKE, FAKE, None) == 1   # no role
+    assert lib.steel_mix_rate(3, 2, FAKE, 10, FAKE, 10, 256, FAKE, FAKE, None) == 1   # bad vop
+    assert lib.steel_mix_rate(1, 0, None, 10, None, 0, 256, FAKE, FAKE, None) == 1    # no operands
+    assert lib.steel_mix_rate(2, 0, None, 0, None, 10, 256, FAKE, FAKE, None) == 1    # no seed
+    assert lib.steel_mix_rate(3, 1, FAKE, 10, FAKE, 10, 0, FAKE, FAKE, None) == 1     # empty grid
     assert lib.steel_lds_rate(3, 10, 256, 4, FAKE, FAKE, None) == 1
     assert lib.steel_lds_rate(0, 0, 256, 4, FAKE, FAKE, None) == 1
     assert lib.steel_lds_rate(0, 10, 256, 17, FAKE, FAKE, None) == 1
