@@ -5,10 +5,12 @@
 //
 // Same mathematics as k_attn (the online-softmax recurrence of Algorithm 1
 // over the live tiles of a query block, Section IV-A masking, Section IV-C
-// work order).  The schedule is built around one property of the CDNA4
-// SIMD: the matrix-core work of a wave holds that wave's instruction issue,
-// so a wave's own exponentials cannot run beside its own MFMAs; only another
-// wave on the same SIMD can fill those cycles.  Algorithm 1 has three stages
+// work order).  The schedule is built around how a CDNA4 SIMD issues: a
+// wave issues in order, one VALU instruction every 8-16 cycles on its own,
+// and an MFMA waits for the SIMD's matrix core, so a wave that mixes score
+// MFMAs into its softmax stalls whenever another wave's MFMAs hold the
+// matrix core.  Kept apart, one wave's softmax runs while the matrix core
+// serves the other wave's MFMAs.  Algorithm 1 has three stages
 // (scores, softmax, P V); the paper places them on separate AIE cores, here
 // they go to two waves of one SIMD that hand P over through LDS:
 //
