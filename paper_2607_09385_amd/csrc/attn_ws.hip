@@ -309,6 +309,22 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
         crow[nt] = a.c / sq * dk;
       }
     };
+    // bf16: Q rows scaled by c = scale * log2(e) and rounded to bf16 at the
+    // item's first tile, so the score MFMAs yield log2 units directly, and
+    // the accumulators start from -m (the row's running maximum, 0 while it
+    // is -inf; nm holds it as a full accumulator tile per N-tile and changes
+    // only when m moves): the common tile needs no per-element fma before
+    // its exponentials
+    constexpr bool MFOLD = PREC == kBf16;
+    f32x16 nm[2];
+    auto scale_q = [&]() __attribute__((always_inline)) {
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qf[nt][ks][e] = (__bf16)((float)qf[nt][ks][e] * a.c);
+    };
     auto skip = [&](const Item&) __attribute__((always_inline)) {};
     have_x = next_nonempty(0, X, jx, skip);
     if (have_x) have_y = next_nonempty(jx + 1, Y, jy, skip);
@@ -346,6 +362,11 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
           ls[0] = 0.f;
           ls[1] = 0.f;
           if constexpr (QK8) quant_q(X);
+          if constexpr (MFOLD) {
+            scale_q();
+            nm[0] = f32x16{};
+            nm[1] = f32x16{};
+          }
         }
         // S^T = K Q^T: for each K fragment (keys 32 sg .. +31, k-step ks) the
         // two N-tiles; fragments read two ahead
@@ -368,7 +389,7 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
             constexpr int q = s >> 1, nt = s & 1;  // q = 2*ks + sg
             if constexpr (nt == 0 && q + 2 < 16) kf[(q + 2) % 3] = k_frag(kbase, q + 2);
             sc[nt][q & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                kf[q % 3], qf[nt][q >> 1], q < 2 ? f32x16{} : sc[nt][q & 1], 0, 0, 0);
+                kf[q % 3], qf[nt][q >> 1], q < 2 ? (MFOLD ? nm[nt] : f32x16{}) : sc[nt][q & 1], 0, 0, 0);
           });
         }
         // the item's last tile: Q of the next item (its loads run under the
@@ -406,12 +427,17 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
 #pragma unroll
               for (int r = 0; r < 16; ++r) x = fmaxf(x, sc[nt][sg][r]);
             x = other_half_max(x);
-            mx[nt] = x == -INFINITY ? -INFINITY : x * crow[nt];
+            if constexpr (MFOLD)  // scores relative to msafe, in log2 units
+              mx[nt] = x == -INFINITY ? -INFINITY : x + (m[nt] == -INFINITY ? 0.f : m[nt]);
+            else
+              mx[nt] = x == -INFINITY ? -INFINITY : x * crow[nt];
             grow |= mx[nt] > m[nt] + TAU;
           }
           const bool any = __builtin_amdgcn_ballot_w64(grow) != 0;
+          float mold[2];
 #pragma unroll
           for (int nt = 0; nt < 2; ++nt) {
+            mold[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
             if (any) {
               const float mnew = fmaxf(m[nt], mx[nt]);
               alpha[nt] = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m[nt] - mnew);
@@ -419,6 +445,17 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
               if constexpr (PV8) ls[nt] *= alpha[nt];
             }
             msafe[nt] = m[nt] == -INFINITY ? 0.f : m[nt];
+          }
+          if constexpr (MFOLD) {
+            if (any) {  // rare: the scores move to the new maximum, and so does nm
+#pragma unroll
+              for (int nt = 0; nt < 2; ++nt) {
+                const float d = mold[nt] - msafe[nt];
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg) sc[nt][sg] += d;
+                nm[nt] = -msafe[nt] + f32x16{};
+              }
+            }
           }
         }
         if constexpr (PV8) {
@@ -466,7 +503,8 @@ __global__ __launch_bounds__(512, 1) void k_attn_ws(AttnArgs a) {
 #pragma unroll
               for (int e = 0; e < 8; ++e)
                 pa[nt][ch][e] = (__bf16)__builtin_amdgcn_exp2f(
-                    __builtin_fmaf(sc[nt][ch >> 1][8 * (ch & 1) + e], a.c, -msafe[nt]));
+                    MFOLD ? sc[nt][ch >> 1][8 * (ch & 1) + e]
+                          : __builtin_fmaf(sc[nt][ch >> 1][8 * (ch & 1) + e], a.c, -msafe[nt]));
               *(bf16x8*)(pdst + (nt * 4 + ch) * 1024) = pa[nt][ch];
               __builtin_amdgcn_sched_barrier(0);
             }
